@@ -1,0 +1,291 @@
+"""Plain float64 oracle for attention BoB (test infrastructure only).
+
+Parity pins live in the CPU test suite; see the module docstring of
+``oracle`` for who may use this file.  Notation follows the paper:
+tau is the softmax scale, U_Q, U_K, U_V are the cotangents on the
+first-backward outputs (dQ, dK, dV), and the BoB outputs are
+Qt, Kt, Vt, dOt (the paper's tilde-Q, tilde-K, tilde-V, tilde-dO).
+
+Layout: every matrix argument is [..., N, d] (any leading batch/head
+dims); row vectors (L, D, alpha, E) are [..., N].  The *_head functions
+take a single head ([N, d]) and are the definitions; the batched wrappers
+loop over leading dims.
+
+Each step is a small named function so a reader can check it against the
+paper line by line, and so the CPU tests can perturb a single step to show
+that the pins catch the mistake.
+"""
+import numpy as np
+
+# --------------------------------------------------------------------------
+# Forward attention (Sec. 2, eq. 1; L as defined in the FlashAttention
+# paragraph of Sec. 2 and in the notation table, App. "Notation").
+# --------------------------------------------------------------------------
+
+
+def scores(q, k, tau):
+    """S = tau * Q K^T (eq. 1, no mask: non-causal dense attention)."""
+    return tau * (q @ k.T)
+
+
+def log_normalizer(S):
+    """L_i = log sum_j exp(S_ij), computed max-subtracted."""
+    m = S.max(axis=-1)
+    return m + np.log(np.exp(S - m[:, None]).sum(axis=-1))
+
+
+def probabilities(S, L):
+    """P_ij = exp(S_ij - L_i): row softmax recomputed from the saved L."""
+    return np.exp(S - L[:, None])
+
+
+def forward_head(q, k, v, tau):
+    """Eq. 1: S = tau Q K^T, P = softmax(S), O = P V; plus L.
+
+    Returns (O, L, P, S).
+    """
+    S = scores(q, k, tau)
+    L = log_normalizer(S)
+    P = probabilities(S, L)
+    O = P @ v
+    return O, L, P, S
+
+
+# --------------------------------------------------------------------------
+# First backward (Sec. 2, eqs. 2-3).
+# --------------------------------------------------------------------------
+
+
+def dP_of(do, v):
+    """dP = dO V^T (eq. 2)."""
+    return do @ v.T
+
+
+def row_D(P, dP):
+    """D_i = sum_j P_ij dP_ij (the row scalar after eq. 3)."""
+    return (P * dP).sum(axis=-1)
+
+
+def dS_of(P, dP, D):
+    """dS_ij = P_ij (dP_ij - D_i) (eq. 2)."""
+    return P * (dP - D[:, None])
+
+
+def first_backward_head(q, k, v, do, tau):
+    """Eqs. 2-3 on one head, materialised.
+
+    Returns a dict with O, L, P, S, dP, D, dS, dQ, dK, dV.
+    """
+    O, L, P, S = forward_head(q, k, v, tau)
+    dP = dP_of(do, v)
+    D = row_D(P, dP)
+    dS = dS_of(P, dP, D)
+    return dict(
+        O=O, L=L, P=P, S=S, dP=dP, D=D, dS=dS,
+        dQ=tau * (dS @ k),          # eq. 3
+        dK=tau * (dS.T @ q),        # eq. 3
+        dV=P.T @ do,                # eq. 2
+    )
+
+
+# --------------------------------------------------------------------------
+# BoB closed form (Sec. 3.2 eqs. 6-7 with the definitions that follow them;
+# the same list appears as "Final assembled identities" in App. A).
+# --------------------------------------------------------------------------
+
+
+def F_of(q, k, uq, uk, tau):
+    """F = tau (U_Q K^T + Q U_K^T): BoB gradient at dS (App. A step 1)."""
+    return tau * (uq @ k.T + q @ uk.T)
+
+
+def C_of(do, uv):
+    """C = dO U_V^T: contribution to tilde-P from the dV child (App. A step 4)."""
+    return do @ uv.T
+
+
+def alpha_of(P, F):
+    """alpha_i = sum_j P_ij F_ij (App. A step 2)."""
+    return (P * F).sum(axis=-1)
+
+
+def Ptilde_of(C, F, dP, D, alpha):
+    """tilde-P_ij = C_ij + F_ij (dP_ij - D_i) - alpha_i dP_ij (App. A step 5)."""
+    return C + F * (dP - D[:, None]) - alpha[:, None] * dP
+
+
+def E_of(P, Pt):
+    """E_i = sum_j P_ij tilde-P_ij (App. A step 6)."""
+    return (P * Pt).sum(axis=-1)
+
+
+def Stilde_of(P, Pt, E):
+    """tilde-S = P (.) (tilde-P - E 1^T) (App. A step 6)."""
+    return P * (Pt - E[:, None])
+
+
+def bob_head(q, k, v, do, uq, uk, uv, tau):
+    """All four BoB outputs on one head, eqs. 6-7, fully materialised.
+
+    Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
+    O, L, D, dQ, dK, dV.
+    """
+    fb = first_backward_head(q, k, v, do, tau)
+    P, dP, D, dS = fb["P"], fb["dP"], fb["D"], fb["dS"]
+    F = F_of(q, k, uq, uk, tau)
+    alpha = alpha_of(P, F)
+    h = F - alpha[:, None]
+    C = C_of(do, uv)
+    Pt = Ptilde_of(C, F, dP, D, alpha)
+    E = E_of(P, Pt)
+    St = Stilde_of(P, Pt, E)
+    Ph = P * h
+    return dict(
+        Qt=tau * (St @ k + dS @ uk),        # eq. 6
+        Kt=tau * (St.T @ q + dS.T @ uq),    # eq. 6
+        Vt=Ph.T @ do,                       # eq. 7
+        dOt=P @ uv + Ph @ v,                # eq. 7
+        alpha=alpha, E=E,
+        O=fb["O"], L=fb["L"], D=D, dQ=fb["dQ"], dK=fb["dK"], dV=fb["dV"],
+    )
+
+
+def bob_affine_head(q, k, v, do, uq, uk, uv, tau):
+    """Row-owned outputs through the affine fusion of Prop. 3.1 (eq. 8).
+
+    The six row accumulators are the sums named in the proof of Prop. 3.1
+    (App. B): alpha, E0 = sum P Pt0, dOt0 = P U_V + (P F) V,
+    Omega = (P Pt0) K + (P (dP - D)) U_K, B = P K, R = (P dP) K, with the
+    alpha-free Pt0 = C + F (dP - D).  The corrections of eq. 8 then give
+    E, dOt and Qt.  Here the sums run over the whole row at once (no tiling),
+    so this is a second route to the same numbers, not the tiled schedule.
+    """
+    O, L, P, _ = forward_head(q, k, v, tau)
+    dP = dP_of(do, v)
+    D = row_D(P, dP)
+    F = F_of(q, k, uq, uk, tau)
+    C = C_of(do, uv)
+    Pt0 = C + F * (dP - D[:, None])
+    alpha = (P * F).sum(axis=-1)
+    E0 = (P * Pt0).sum(axis=-1)
+    dOt0 = P @ uv + (P * F) @ v
+    Omega = (P * Pt0) @ k + (P * (dP - D[:, None])) @ uk
+    Bacc = P @ k
+    R = (P * dP) @ k
+    E = E0 - alpha * D
+    dOt = dOt0 - alpha[:, None] * O
+    Qt = tau * (Omega - alpha[:, None] * R - E[:, None] * Bacc)
+    return dict(Qt=Qt, dOt=dOt, alpha=alpha, E=E, E0=E0)
+
+
+# --------------------------------------------------------------------------
+# An independently written first backward g(Q, K, V, dO) = (dQ, dK, dV):
+# one query row at a time, the softmax Jacobian written out as
+# diag(p) - p p^T (App. A step 6 derives it by the quotient rule).
+# It shares no helper with the functions above and exists so that finite
+# differences of Phi = <dQ,U_Q> + <dK,U_K> + <dV,U_V> (eq. 4) give an
+# independent check of every BoB output (eq. 5).
+# --------------------------------------------------------------------------
+
+
+def first_backward_rowloop(q, k, v, do, tau):
+    n, d = q.shape
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for i in range(n):
+        s = np.array([tau * float(np.dot(q[i], k[j])) for j in range(n)])
+        e = np.exp(s - s.max())
+        p = e / e.sum()
+        grad_p = v @ do[i]                      # d<o_i, do_i>/dp_j = v_j . do_i
+        jac = np.diag(p) - np.outer(p, p)       # dp/ds for one softmax row
+        grad_s = jac.T @ grad_p
+        dq[i] = tau * (grad_s @ k)
+        dk += tau * np.outer(grad_s, q[i])
+        dv += np.outer(p, do[i])
+    return dq, dk, dv
+
+
+def phi_rowloop(q, k, v, do, uq, uk, uv, tau):
+    """Phi of eq. 4 evaluated through the independent first backward."""
+    dq, dk, dv = first_backward_rowloop(q, k, v, do, tau)
+    return float((dq * uq).sum() + (dk * uk).sum() + (dv * uv).sum())
+
+
+# --------------------------------------------------------------------------
+# Batched wrappers: leading dims are independent heads (Sec. 2, "the analysis
+# extends naturally to multiple heads").
+# --------------------------------------------------------------------------
+
+
+def _heads(x):
+    return x.reshape((-1,) + x.shape[-2:])
+
+
+def _batched(fn, keys, shapes_from, *mats, tau):
+    lead = shapes_from.shape[:-2]
+    flat = [_heads(np.asarray(m, dtype=np.float64)) for m in mats]
+    outs = [fn(*[m[h] for m in flat], tau) for h in range(flat[0].shape[0])]
+    res = {}
+    for key in keys:
+        arr = np.stack([o[key] for o in outs])
+        res[key] = arr.reshape(lead + arr.shape[1:])
+    return res
+
+
+def forward(Q, K, V, tau):
+    """Batched eq. 1: returns dict(O, L)."""
+    def f(q, k, v, t):
+        O, L, _, _ = forward_head(q, k, v, t)
+        return dict(O=O, L=L)
+    return _batched(f, ("O", "L"), Q, Q, K, V, tau=tau)
+
+
+def first_backward(Q, K, V, dO, tau):
+    """Batched eqs. 1-3: returns dict(O, L, D, dQ, dK, dV)."""
+    keys = ("O", "L", "D", "dQ", "dK", "dV")
+    return _batched(first_backward_head, keys, Q, Q, K, V, dO, tau=tau)
+
+
+def bob(Q, K, V, dO, UQ, UK, UV, tau):
+    """Batched BoB (eqs. 6-7): dict(Qt, Kt, Vt, dOt, alpha, E, O, L, D, dQ, dK, dV)."""
+    keys = ("Qt", "Kt", "Vt", "dOt", "alpha", "E", "O", "L", "D", "dQ", "dK", "dV")
+    return _batched(bob_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau)
+
+
+def bob_affine(Q, K, V, dO, UQ, UK, UV, tau):
+    """Batched Prop. 3.1 route: dict(Qt, dOt, alpha, E, E0)."""
+    keys = ("Qt", "dOt", "alpha", "E", "E0")
+    return _batched(bob_affine_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau)
+
+
+def bob_rows(q, k, v, do, uq, uk, uv, tau, rows):
+    """Row-owned outputs of one head restricted to the query rows `rows`.
+
+    Every row-owned quantity (Qt, dOt, alpha, E, O, L, D, dQ) of row i depends
+    only on row i of the N x N matrices (Sec. 3.2: they "sum over columns for
+    each fixed row"), so the same definitions applied to a slab of query rows
+    give exactly those rows.  Used for large N, where the full N x N matrices
+    do not fit.
+    """
+    rows = np.asarray(rows)
+    qi, doi, uqi = q[rows], do[rows], uq[rows]
+    S = scores(qi, k, tau)
+    L = log_normalizer(S)
+    P = probabilities(S, L)
+    O = P @ v
+    dP = dP_of(doi, v)
+    D = row_D(P, dP)
+    dS = dS_of(P, dP, D)
+    F = F_of(qi, k, uqi, uk, tau)
+    alpha = alpha_of(P, F)
+    h = F - alpha[:, None]
+    C = C_of(doi, uv)
+    Pt = Ptilde_of(C, F, dP, D, alpha)
+    E = E_of(P, Pt)
+    St = Stilde_of(P, Pt, E)
+    return dict(
+        Qt=tau * (St @ k + dS @ uk),
+        dOt=P @ uv + (P * h) @ v,
+        alpha=alpha, E=E, O=O, L=L, D=D, dQ=tau * (dS @ k),
+    )

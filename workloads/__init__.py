@@ -1,0 +1,73 @@
+"""Seeded synthetic inputs for attention BoB (shared by tests, bench and smoke).
+
+This module holds no arithmetic of the method: it only draws the seven
+[B, H, N, d] input tensors (Q, K, V, dO and the cotangents U_Q, U_K, U_V on
+the first-backward outputs) and names the workload shapes.  Both the HIP
+path and the float64 oracle consume the exact values it returns.
+
+Recipe (the same for every workload): a CPU ``torch.Generator`` seeded with
+``seed`` draws float32 standard normals of shape [B, H, N, d] in the order
+Q, K, V, dO, U_Q, U_K, U_V; Q and K are then multiplied by ``qk_scale`` in
+float32; finally every tensor is cast to the workload dtype with
+round-to-nearest-even.  The softmax scale is 1/sqrt(d).
+"""
+from dataclasses import dataclass
+import math
+
+import torch
+
+NAMES = ("Q", "K", "V", "dO", "UQ", "UK", "UV")
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    N: int
+    d: int
+    dtype: str          # "f32" or "bf16"
+    seed: int
+    qk_scale: float = 1.0
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.d)
+
+    @property
+    def torch_dtype(self):
+        return torch.float32 if self.dtype == "f32" else torch.bfloat16
+
+
+# The five workloads: a tiny fp32 case, a small bf16 case, the N=16K d=128
+# case, a long-context N=64K case and the N=256K maximum-length case.
+WORKLOADS = {
+    "tiny_f32_n256_d64": Workload("tiny_f32_n256_d64", 1, 1, 256, 64, "f32", 0),
+    "bf16_b2h8_n4096_d64": Workload("bf16_b2h8_n4096_d64", 2, 8, 4096, 64, "bf16", 1),
+    "bf16_b1h16_n16384_d128": Workload("bf16_b1h16_n16384_d128", 1, 16, 16384, 128, "bf16", 2, 0.5),
+    "bf16_b1h8_n65536_d64": Workload("bf16_b1h8_n65536_d64", 1, 8, 65536, 64, "bf16", 3),
+    "bf16_b1h4_n262144_d64": Workload("bf16_b1h4_n262144_d64", 1, 4, 262144, 64, "bf16", 4),
+}
+
+
+def make_inputs(B, H, N, d, dtype="bf16", seed=0, qk_scale=1.0, device="cpu"):
+    """Return a dict name -> tensor [B, H, N, d] following the module recipe."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(int(seed))
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    out = {}
+    for name in NAMES:
+        x = torch.randn((B, H, N, d), generator=gen, dtype=torch.float32)
+        if name in ("Q", "K") and qk_scale != 1.0:
+            x = x * qk_scale
+        out[name] = x.to(tdt).to(device)
+    return out
+
+
+def workload_inputs(w: Workload, device="cpu"):
+    return make_inputs(w.B, w.H, w.N, w.d, w.dtype, w.seed, w.qk_scale, device)
+
+
+def as_f64(t):
+    """Exact float64 NumPy copy of a CPU or device tensor (bf16/f32 upcast is exact)."""
+    return t.detach().to("cpu", torch.float64).numpy()
