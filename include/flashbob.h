@@ -1,0 +1,112 @@
+/*
+ * flashbob.h -- C ABI of libflashbob.so: exact backward-over-backward (BoB)
+ * for softmax attention on AMD Instinct MI355X (gfx950).
+ *
+ * The method is FlashBoB (arXiv 2609.24089).  Given Q, K, V, dO and
+ * cotangents U_Q, U_K, U_V on the first-backward outputs (dQ, dK, dV), BoB
+ * returns the gradients of Phi = <dQ,U_Q> + <dK,U_K> + <dV,U_V> with respect
+ * to Q, K, V and dO (Sec. 3.1, eqs. 4-5).  The library computes them with
+ * the two-pass schedule of Alg. 1: Pass 1 holds a block of query rows and
+ * streams key blocks, finishing alpha, E, Qt and dOt through the affine
+ * fusion of Prop. 3.1 (eq. 8); Pass 2 holds a block of key rows and streams
+ * query blocks, finishing Kt and Vt.  The forward (eq. 1) and first backward
+ * (eqs. 2-3) that produce the row state (O, L, D) are provided as well.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  dtype   BOB_F32 (fp32 tensors, fp32 arithmetic throughout) or BOB_BF16
+ *          (bf16 tensors; bf16 MFMA operands with fp32 accumulation; fp32
+ *          row scalars and elementwise math; outputs rounded to nearest even).
+ *  B, H, N, d  batch, heads, sequence length and head dimension.  Matrices
+ *          are contiguous row-major [B, H, N, d] in the tensor dtype; row
+ *          vectors (L, D, alpha, E) are contiguous fp32 [B, H, N].
+ *          Supported head dimensions: d = 64 and d = 128 (both dtypes).
+ *  scale   the softmax scale tau of eq. 1 (the paper uses 1/sqrt(d)); any
+ *          finite value is accepted.  L is the natural-log normalizer
+ *          L_i = log sum_j exp(S_ij) with S = tau Q K^T.  No mask: every key
+ *          is visible to every query (dense, non-causal attention).
+ *  pointers  device pointers owned by the caller, 16-byte aligned.  The
+ *          library allocates no memory and keeps no state.  Outputs must not
+ *          alias inputs.
+ *  stream  a hipStream_t passed as void* (NULL = the default stream).  Work
+ *          is enqueued asynchronously; the call returns before it finishes.
+ *          Calls that consume another call's outputs (attn_bwd after
+ *          attn_fwd_lse, pass 2 after pass 1) must be ordered on one stream
+ *          or with events by the caller.
+ *
+ * Errors: every argument check happens before any HIP call, so a rejected
+ * call has no effect.  BOB_EINVAL: negative B/H/N, non-finite scale, a NULL
+ * or misaligned pointer for a non-empty problem, or a problem too large for
+ * the launch grid.  BOB_EUNSUPPORTED: a (dtype, d) pair that is not built.
+ * BOB_ELAUNCH: the HIP launch itself reported an error.  B*H*N == 0 is a
+ * valid empty problem and returns BOB_OK without touching memory.  No
+ * exception crosses the ABI and the library never aborts.
+ */
+#ifndef FLASHBOB_H
+#define FLASHBOB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { BOB_F32 = 0, BOB_BF16 = 1 } bob_dtype;
+
+typedef enum {
+  BOB_OK = 0,
+  BOB_EINVAL = 1,
+  BOB_EUNSUPPORTED = 2,
+  BOB_ELAUNCH = 3
+} bob_status;
+
+/* Forward attention (eq. 1) with its log-normalizer (Sec. 2).
+ * In:  Q, K, V  [B,H,N,d].
+ * Out: O = softmax(scale Q K^T) V  [B,H,N,d];  L (fp32 [B,H,N]). */
+int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                     const void* Q, const void* K, const void* V,
+                     void* O, float* L, void* stream);
+
+/* First backward (eqs. 2-3) from the saved forward state.
+ * In:  Q, K, V, O, dO [B,H,N,d];  L fp32 [B,H,N] from attn_fwd_lse.
+ * Out: dQ, dK, dV [B,H,N,d];  D fp32 [B,H,N], D_i = do_i . o_i.
+ * D is written by the row kernel before the column kernel reads it (both
+ * are enqueued on `stream` by this call). */
+int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                 const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* L, void* dQ, void* dK, void* dV, float* D, void* stream);
+
+/* BoB Pass 1, row-major (Alg. 1 Pass 1; Prop. 3.1 and eq. 8).
+ * In:  Q, K, V, O, dO, gdQ (= U_Q), gdK (= U_K), gdV (= U_V) [B,H,N,d];
+ *      L, D fp32 [B,H,N] from attn_fwd_lse / attn_bwd.
+ * Out: Qt, dOt [B,H,N,d];  alpha, E fp32 [B,H,N] -- the two row scalars
+ *      alpha_i = sum_j P_ij F_ij and E_i = sum_j P_ij Pt_ij that Pass 2 reads. */
+int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                            const void* Q, const void* K, const void* V, const void* O,
+                            const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                            const float* L, const float* D,
+                            void* Qt, void* dOt, float* alpha, float* E, void* stream);
+
+/* BoB Pass 2, column-major (Alg. 1 Pass 2).
+ * In:  Q, K, V, dO, gdQ, gdK, gdV [B,H,N,d];  L, D, alpha, E fp32 [B,H,N].
+ * Out: Kt, Vt [B,H,N,d].  Must run after Pass 1 has written alpha and E. */
+int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                            const void* Q, const void* K, const void* V, const void* dO,
+                            const void* gdQ, const void* gdK, const void* gdV,
+                            const float* L, const float* D, const float* alpha, const float* E,
+                            void* Kt, void* Vt, void* stream);
+
+/* 1 if (dtype, d) is built into this library, else 0. */
+int32_t bob_supported(int32_t dtype, int64_t d);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char* bob_status_string(int32_t status);
+
+/* Static version string of the library. */
+const char* bob_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHBOB_H */

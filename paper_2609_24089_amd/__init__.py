@@ -1,0 +1,164 @@
+"""Exact attention backward-over-backward (FlashBoB) on MI355X.
+
+Thin Python binding over libflashbob.so (include/flashbob.h).  The four entry
+points keep the C names; each one only checks and marshals torch-ROCm tensors
+(device memory and the current stream) and calls the library, so every step
+of the computation runs in the gfx950 kernels.  There is no fallback: if the
+library is missing, importing the binding raises.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libflashbob.so")
+
+BOB_F32 = 0
+BOB_BF16 = 1
+BOB_OK, BOB_EINVAL, BOB_EUNSUPPORTED, BOB_ELAUNCH = 0, 1, 2, 3
+
+_lib = None
+
+
+def load_library():
+    """Load libflashbob.so (built by paper_2609_24089_amd.build); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2609_24089_amd.build` "
+            "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+    common = [i32, i64, i64, i64, i64, f32]
+    lib.attn_fwd_lse.argtypes = common + [vp] * 5 + [vp]
+    lib.attn_bwd.argtypes = common + [vp] * 10 + [vp]
+    lib.attn_bob_pass1_rows.argtypes = common + [vp] * 14 + [vp]
+    lib.attn_bob_pass2_cols.argtypes = common + [vp] * 13 + [vp]
+    for fn in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"):
+        getattr(lib, fn).restype = i32
+    lib.bob_supported.argtypes = [i32, i64]
+    lib.bob_supported.restype = i32
+    lib.bob_status_string.argtypes = [i32]
+    lib.bob_status_string.restype = ctypes.c_char_p
+    lib.bob_version.argtypes = []
+    lib.bob_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(rc):
+    return load_library().bob_status_string(int(rc)).decode()
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return BOB_BF16
+    if t.dtype == torch.float32:
+        return BOB_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; expected torch.bfloat16 or torch.float32")
+
+
+def _check_mats(*ts):
+    ref = ts[0]
+    if ref.dim() != 4:
+        raise ValueError("matrices must be [B, H, N, d]")
+    for t in ts:
+        if t.shape != ref.shape or t.dtype != ref.dtype or t.device != ref.device:
+            raise ValueError("all matrices must share shape, dtype and device")
+        if not t.is_contiguous():
+            raise ValueError("matrices must be contiguous")
+        if t.device.type != "cuda":
+            raise ValueError("matrices must be on a ROCm device")
+    return ref.shape
+
+
+def _check_rows(shape, *vs):
+    for v in vs:
+        if v.dtype != torch.float32 or tuple(v.shape) != tuple(shape[:3]) or not v.is_contiguous():
+            raise ValueError("row vectors must be contiguous float32 [B, H, N]")
+
+
+def _p(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _call(fn, *args):
+    rc = fn(*args)
+    if rc != BOB_OK:
+        raise RuntimeError(status_string(rc))
+
+
+def _rows_empty(shape, like):
+    return torch.empty(tuple(shape[:3]), dtype=torch.float32, device=like.device)
+
+
+def attn_fwd_lse(Q, K, V, scale, stream=None):
+    """Forward attention (eq. 1): returns (O, L)."""
+    B, H, N, d = _check_mats(Q, K, V)
+    O = torch.empty_like(Q)
+    L = _rows_empty(Q.shape, Q)
+    lib = load_library()
+    _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale),
+          _p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
+    return O, L
+
+
+def attn_bwd(Q, K, V, O, dO, L, scale, stream=None):
+    """First backward (eqs. 2-3): returns (dQ, dK, dV, D)."""
+    B, H, N, d = _check_mats(Q, K, V, O, dO)
+    _check_rows(Q.shape, L)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q)
+    D = _rows_empty(Q.shape, Q)
+    lib = load_library()
+    _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale),
+          _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
+    return dQ, dK, dV, D
+
+
+def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, out=None, stream=None):
+    """BoB Pass 1 (row-major): returns (Qt, dOt, alpha, E)."""
+    B, H, N, d = _check_mats(Q, K, V, O, dO, gdQ, gdK, gdV)
+    _check_rows(Q.shape, L, D)
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q), _rows_empty(Q.shape, Q))
+    Qt, dOt, alpha, E = out
+    lib = load_library()
+    _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale),
+          _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
+          _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
+    return Qt, dOt, alpha, E
+
+
+def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, out=None, stream=None):
+    """BoB Pass 2 (column-major): returns (Kt, Vt)."""
+    B, H, N, d = _check_mats(Q, K, V, dO, gdQ, gdK, gdV)
+    _check_rows(Q.shape, L, D, alpha, E)
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(Q))
+    Kt, Vt = out
+    lib = load_library()
+    _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale),
+          _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
+          _p(Kt), _p(Vt), _stream(stream))
+    return Kt, Vt
+
+
+def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, stream=None):
+    """Whole path: forward, first backward, Pass 1, Pass 2 on one stream.
+
+    Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
+    O, L, D, dQ, dK, dV.
+    """
+    O, L = attn_fwd_lse(Q, K, V, scale, stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, stream)
+    Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, stream=stream)
+    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, stream=stream)
+    return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)

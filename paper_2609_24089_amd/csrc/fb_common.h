@@ -1,0 +1,251 @@
+// Shared device-side building blocks for the attention kernels (gfx950 only).
+//
+// Every kernel in this library has the same shape.  A workgroup owns a block
+// of "stationary" rows (query rows in the row-major kernels, key rows in the
+// column-major kernels), held as MFMA B-operands in registers.  It streams
+// the other side of the attention matrix through LDS in tiles of kBS = 32
+// rows, and per tile it
+//   1. forms transposed score-like tiles  T[s][t] = X_s . Y_t   (s streamed,
+//      t stationary) with v_mfma_f32_16x16x32_bf16 (or 16x16x4f32), where the
+//      streamed row-major tile is the A-operand read straight out of LDS;
+//   2. does the elementwise work on those tiles in fp32 registers (the output
+//      layout puts the stationary row on lane & 15, so row scalars are
+//      per-lane values);
+//   3. accumulates Acc^T[dim][t] += X^T[dim][s] . T^T[s][t], with the
+//      streamed tile transposed on the fly by ds_read_b64_tr_b16 and the
+//      score tile reused in registers as the B-operand.
+// Accumulators therefore live transposed: lane l holds dims 16*nb + 4*(l>>4)
+// + r (r = 0..3) of stationary row 16*mb + (l & 15).
+//
+// Lane layouts (checked on gfx950 with an in-bounds probe):
+//   16x16x32 bf16 A: lane l -> row l&15, k = 8*(l>>4) + e, e = 0..7
+//                 B: lane l -> col l&15, same k;   C: lane l -> rows 4*(l>>4)+r, col l&15
+//   16x16x4 f32   A: lane l -> row l&15, k = l>>4;  B: col l&15, k = l>>4; C as above
+//   ds_read_b64_tr_b16: in each group of 16 lanes, lane j gives the address of
+//   4 consecutive 16-bit elements (row j/4, cols 4*(j%4)..+3 of a 4x16 block);
+//   lane i receives column i of that block (4 elements, rows 0..3).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fb {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define FB_LDS __attribute__((address_space(3)))
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kBS = 32;  // streamed rows per tile (two 16-row MFMA sub-blocks)
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Sum / max over the four lanes that share lane & 15 (the four k-groups).
+__device__ __forceinline__ float group_sum(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+__device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// Element-type policy.  A "chunk" is the 16 bytes one lane contributes to a
+// score MFMA step: 8 bf16 (one 16x16x32 MFMA) or 4 fp32 (four 16x16x4 MFMAs).
+// Lane group g = l >> 4 covers dims [kk*kKC + g*kKC/4, +kKC/4) of chunk kk,
+// i.e. byte offset 64*kk + 16*g in the row, for both element types.
+// ---------------------------------------------------------------------------
+template <typename T> struct Elt;
+
+template <> struct Elt<bf16> {
+  static constexpr int kKC = 32;
+  // score step over one chunk
+  static __device__ __forceinline__ floatx4 mma_chunk(u32x4 a, u32x4 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+  // A-operand of the accumulate step: 16 dims x 32 streamed rows, transposed
+  struct AFrag { bf16x8 v; };
+  // B-operand of the accumulate step: this lane's stationary row against the
+  // 8 streamed rows {4g+r, 16+4g+r}; slot i = 4*h + r
+  struct TFrag {
+    bf16x8 v;
+    __device__ __forceinline__ void set(int i, float x) { v[i] = (bf16)x; }
+  };
+  static __device__ __forceinline__ AFrag load_afrag(const bf16 FB_LDS* X, int ldx, int dim0) {
+    const int l = lane_id(), g = l >> 4, j = l & 15;
+    const bf16 FB_LDS* p = X + (4 * g + (j >> 2)) * ldx + dim0 + 4 * (j & 3);
+    shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)p);
+    shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)(p + 16 * ldx));
+    AFrag a;
+    a.v = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    return a;
+  }
+  static __device__ __forceinline__ floatx4 mma_acc(const AFrag& a, const TFrag& b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
+  }
+  // store 4 consecutive output elements (fp32 -> bf16, round to nearest even)
+  static __device__ __forceinline__ void store4(bf16* p, floatx4 x) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 y;
+    y[0] = (bf16)x[0]; y[1] = (bf16)x[1]; y[2] = (bf16)x[2]; y[3] = (bf16)x[3];
+    *(u32x2*)p = __builtin_bit_cast(u32x2, y);
+  }
+  static __device__ __forceinline__ floatx4 load4(const bf16* p) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 y = __builtin_bit_cast(bf16x4, *(const u32x2*)p);
+    return floatx4{(float)y[0], (float)y[1], (float)y[2], (float)y[3]};
+  }
+  // dot product of two chunks (used for D = rowsum(dO * O))
+  static __device__ __forceinline__ float dot_chunk(u32x4 a, u32x4 b) {
+    bf16x8 x = __builtin_bit_cast(bf16x8, a), y = __builtin_bit_cast(bf16x8, b);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s = __builtin_fmaf((float)x[e], (float)y[e], s);
+    return s;
+  }
+};
+
+template <> struct Elt<float> {
+  static constexpr int kKC = 16;
+  // The chunk is reinterpreted as a whole floatx4 before taking elements:
+  // bit-casting single u32 vector elements inside an unrolled loop made this
+  // compiler feed element 0 to every MFMA.
+  static __device__ __forceinline__ floatx4 mma_chunk(u32x4 a, u32x4 b, floatx4 c) {
+    const floatx4 x = __builtin_bit_cast(floatx4, a), y = __builtin_bit_cast(floatx4, b);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[0], y[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[1], y[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[2], y[2], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[3], y[3], c, 0, 0, 0);
+    return c;
+  }
+  struct AFrag { float v[8]; };
+  struct TFrag {
+    float v[8];
+    __device__ __forceinline__ void set(int i, float x) { v[i] = x; }
+  };
+  static __device__ __forceinline__ AFrag load_afrag(const float FB_LDS* X, int ldx, int dim0) {
+    const int l = lane_id(), g = l >> 4, j = l & 15;
+    AFrag a;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a.v[4 * h + r] = X[(16 * h + 4 * g + r) * ldx + dim0 + j];
+    return a;
+  }
+  static __device__ __forceinline__ floatx4 mma_acc(const AFrag& a, const TFrag& b, floatx4 c) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[i], b.v[i], c, 0, 0, 0);
+    return c;
+  }
+  static __device__ __forceinline__ void store4(float* p, floatx4 x) { *(floatx4*)p = x; }
+  static __device__ __forceinline__ floatx4 load4(const float* p) { return *(const floatx4*)p; }
+  static __device__ __forceinline__ float dot_chunk(u32x4 a, u32x4 b) {
+    const floatx4 x = __builtin_bit_cast(floatx4, a), y = __builtin_bit_cast(floatx4, b);
+    return __builtin_fmaf(x[3], y[3], __builtin_fmaf(x[2], y[2], __builtin_fmaf(x[1], y[1], x[0] * y[0])));
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Geometry helpers
+// ---------------------------------------------------------------------------
+template <typename T, int D> struct Geo {
+  static constexpr int kChunks = D * (int)sizeof(T) / 64;       // score chunks per row (per lane group)
+  static constexpr int kCPR = D * (int)sizeof(T) / 16;          // 16-byte chunks per row
+  static constexpr int kPad = 16 / (int)sizeof(T);              // +16 bytes per LDS row
+  static constexpr int kLdx = D + kPad;                          // LDS row stride (elements)
+  static constexpr int kTileElems = kBS * kLdx;                  // one streamed tile in LDS
+  static constexpr int kNB = D / 16;                             // 16-dim output blocks
+  static __device__ __forceinline__ int chunk_elem(int kk, int g) { return kk * Elt<T>::kKC + g * (Elt<T>::kKC / 4); }
+};
+
+// Map a workgroup to (head, row block).  Workgroups are dispatched round-robin
+// over the 8 XCDs; when the count allows it, consecutive logical blocks (which
+// stream the same head's tensors) are kept on one XCD so they share its L2.
+__device__ __forceinline__ void map_block(int nRB, int total, int& bh, int& rb) {
+  int wg = blockIdx.x;
+  int logical = ((total & 7) == 0) ? (wg & 7) * (total >> 3) + (wg >> 3) : wg;
+  bh = logical / nRB;
+  rb = logical - bh * nRB;
+}
+
+// Load the B-operand chunks of one stationary 16-row block: lane l holds row
+// row0 + (l & 15), chunk kk at dims chunk_elem(kk, l >> 4).  Rows >= N read 0.
+template <typename T, int D, int NC>
+__device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, int row, int N) {
+  static_assert(NC == Geo<T, D>::kChunks, "chunk count");
+  const int g = lane_id() >> 4;
+#pragma unroll
+  for (int kk = 0; kk < NC; ++kk) {
+    if (row < N)
+      f[kk] = *(const u32x4*)(head + (int64_t)row * D + Geo<T, D>::chunk_elem(kk, g));
+    else
+      f[kk] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// Register-staged copy of NTENS streamed tiles (kBS rows x D each) from HBM to
+// LDS.  Rows >= N are zero-filled.  NT = threads in the workgroup.
+template <typename T, int D, int NT, int NTENS>
+struct TileCopy {
+  static constexpr int kCPR = Geo<T, D>::kCPR;
+  static constexpr int kNCH = kBS * kCPR;                       // chunks per tensor tile
+  static constexpr int kPer = (kNCH + NT - 1) / NT;
+  u32x4 r[NTENS][kPer];
+
+  __device__ __forceinline__ void load(const T* const (&src)[NTENS], int s0, int N) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int row = c / kCPR, col = c - row * kCPR;
+      const bool ok = (c < kNCH) && (s0 + row < N);
+#pragma unroll
+      for (int t = 0; t < NTENS; ++t) {
+        if (ok)
+          r[t][i] = *(const u32x4*)(src[t] + (int64_t)(s0 + row) * D + col * (16 / (int)sizeof(T)));
+        else
+          r[t][i] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  }
+  __device__ __forceinline__ void store(T FB_LDS* dst) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = threadIdx.x + i * NT;
+      if (c < kNCH) {
+        const int row = c / kCPR, col = c - row * kCPR;
+#pragma unroll
+        for (int t = 0; t < NTENS; ++t)
+          *(u32x4 FB_LDS*)(dst + t * Geo<T, D>::kTileElems + row * Geo<T, D>::kLdx + col * (16 / (int)sizeof(T))) = r[t][i];
+      }
+    }
+  }
+};
+
+// Streamed per-row fp32 scalars (L, D, alpha, E) for one tile: NS vectors of
+// kBS floats; entries >= N are zero.
+template <int NS>
+__device__ __forceinline__ void copy_row_scalars(float FB_LDS* dst, const float* const (&src)[NS], int s0, int N) {
+  const int t = threadIdx.x;
+  if (t < NS * kBS) {
+    const int v = t / kBS, i = t - v * kBS;
+    float x = 0.f;
+#pragma unroll
+    for (int u = 0; u < NS; ++u)
+      if (u == v && s0 + i < N) x = src[u][s0 + i];
+    dst[v * kBS + i] = x;
+  }
+}
+
+}  // namespace fb

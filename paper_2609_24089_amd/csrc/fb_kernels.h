@@ -1,0 +1,641 @@
+// Attention forward, first backward and the two BoB passes as gfx950 kernels.
+//
+// Notation follows the paper: tau = softmax scale, U_Q/U_K/U_V are the
+// cotangents on (dQ, dK, dV), and the BoB outputs are Qt, Kt, Vt, dOt
+// (the paper's tilde-Q, tilde-K, tilde-V, tilde-dO).  All matrices are
+// [B*H, N, D] row-major; row scalars L, D, alpha, E are fp32 [B*H, N].
+// Softmax probabilities are recomputed from L as exp2(S*tau*log2e - L*log2e).
+#pragma once
+#include "fb_common.h"
+
+namespace fb {
+
+// ===========================================================================
+// Forward: O = softmax(tau Q K^T) V and L = logsumexp(tau Q K^T)  (eq. 1 and
+// the log-normalizer of Sec. 2).  Stationary: query rows.  Streamed: K, V.
+// Online softmax with a running row max, as in FlashAttention.
+// ===========================================================================
+template <typename T, int D, int MR, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NT = NW * 64;
+  constexpr int BR = 16 * MR * NW;
+  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int row0 = rb * BR + wave_id() * 16 * MR;
+
+  u32x4 qf[MR][G::kChunks];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) load_stationary<T, D>(qf[mb], Q + hoff, row0 + 16 * mb + j, N);
+
+  floatx4 acc[G::kNB][MR];
+#pragma unroll
+  for (int nb = 0; nb < G::kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float mrun[MR], lsum[MR];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) { mrun[mb] = -1e30f; lsum[mb] = 0.f; }
+  const float c = scale * kLog2e;
+
+  TileCopy<T, D, NT, 2> cp;
+  const T* const src[2] = {K + hoff, V + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  cp.load(src, 0, N);
+  cp.store((T FB_LDS*)lds[0]);
+  __syncthreads();
+  for (int it = 0; it < nT; ++it) {
+    const int s0 = it * kBS;
+    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* Vt = Kt + G::kTileElems;
+
+    floatx4 s[2][MR];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int kk = 0; kk < G::kChunks; ++kk) {
+        const u32x4 a = *(const u32x4 FB_LDS*)(Kt + (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g));
+#pragma unroll
+        for (int mb = 0; mb < MR; ++mb) s[sb][mb] = E::mma_chunk(a, qf[mb][kk], s[sb][mb]);
+      }
+
+    typename E::TFrag pf[MR];
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb) {
+      float x[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = s0 + 16 * sb + 4 * g + r < N;
+          x[4 * sb + r] = ok ? s[sb][mb][r] * c : -INFINITY;
+          mx = fmaxf(mx, x[4 * sb + r]);
+        }
+      mx = group_max(mx);
+      const float mnew = fmaxf(mrun[mb], mx);
+      const float corr = fast_exp2(mrun[mb] - mnew);
+      mrun[mb] = mnew;
+      float ls = lsum[mb] * corr;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float p = fast_exp2(x[i] - mnew);
+        ls += p;
+        pf[mb].set(i, p);
+      }
+      lsum[mb] = ls;
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
+    }
+#pragma unroll
+    for (int nb = 0; nb < G::kNB; ++nb) {
+      const typename E::AFrag a = E::load_afrag(Vt, G::kLdx, 16 * nb);
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, pf[mb], acc[nb][mb]);
+    }
+    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    const float lt = group_sum(lsum[mb]);
+    const float inv = 1.f / lt;
+    if (row < N) {
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) E::store4(O + hoff + (int64_t)row * D + 16 * nb + 4 * g, acc[nb][mb] * inv);
+      if (g == 0) L[(int64_t)bh * N + row] = (mrun[mb] + __log2f(lt)) * kLn2;
+    }
+  }
+}
+
+// ===========================================================================
+// First backward, row side: D_i = do_i . o_i and dQ = tau dS K with
+// dS = P (dP - D), dP = dO V^T (eqs. 2-3).  Stationary: Q, dO rows.
+// Streamed: K, V.  Writes D and dQ once per row; no atomics.
+// ===========================================================================
+template <typename T, int D, int MR, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const T* __restrict__ O, const T* __restrict__ dO, const float* __restrict__ L,
+    T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NT = NW * 64;
+  constexpr int BR = 16 * MR * NW;
+  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int row0 = rb * BR + wave_id() * 16 * MR;
+
+  u32x4 qf[MR][G::kChunks], dof[MR][G::kChunks];
+  float lb[MR], drow[MR];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    load_stationary<T, D>(qf[mb], Q + hoff, row, N);
+    load_stationary<T, D>(dof[mb], dO + hoff, row, N);
+    u32x4 of[G::kChunks];
+    load_stationary<T, D>(of, O + hoff, row, N);
+    float part = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < G::kChunks; ++kk) part += E::dot_chunk(dof[mb][kk], of[kk]);
+    drow[mb] = group_sum(part);
+    lb[mb] = row < N ? L[(int64_t)bh * N + row] * kLog2e : 0.f;
+    if (g == 0 && row < N) Dout[(int64_t)bh * N + row] = drow[mb];
+  }
+
+  floatx4 acc[G::kNB][MR];
+#pragma unroll
+  for (int nb = 0; nb < G::kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float c = scale * kLog2e;
+
+  TileCopy<T, D, NT, 2> cp;
+  const T* const src[2] = {K + hoff, V + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  cp.load(src, 0, N);
+  cp.store((T FB_LDS*)lds[0]);
+  __syncthreads();
+  for (int it = 0; it < nT; ++it) {
+    const int s0 = it * kBS;
+    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* Vt = Kt + G::kTileElems;
+
+    floatx4 s[2][MR], dp[2][MR];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int kk = 0; kk < G::kChunks; ++kk) {
+        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const u32x4 ak = *(const u32x4 FB_LDS*)(Kt + off);
+        const u32x4 av = *(const u32x4 FB_LDS*)(Vt + off);
+#pragma unroll
+        for (int mb = 0; mb < MR; ++mb) {
+          s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);
+          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);
+        }
+      }
+    typename E::TFrag dsf[MR];
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = s0 + 16 * sb + 4 * g + r < N;
+          const float p = ok ? fast_exp2(s[sb][mb][r] * c - lb[mb]) : 0.f;
+          dsf[mb].set(4 * sb + r, p * (dp[sb][mb][r] - drow[mb]));
+        }
+#pragma unroll
+    for (int nb = 0; nb < G::kNB; ++nb) {
+      const typename E::AFrag a = E::load_afrag(Kt, G::kLdx, 16 * nb);
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, dsf[mb], acc[nb][mb]);
+    }
+    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    if (row < N) {
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) E::store4(dQ + hoff + (int64_t)row * D + 16 * nb + 4 * g, acc[nb][mb] * scale);
+    }
+  }
+}
+
+// ===========================================================================
+// First backward, column side: dV = P^T dO and dK = tau dS^T Q (eqs. 2-3).
+// Stationary: K, V rows.  Streamed: Q, dO tiles with their L and D.
+// ===========================================================================
+template <typename T, int D, int MC, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
+    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NT = NW * 64;
+  constexpr int BC = 16 * MC * NW;
+  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) float sc[2][2 * kBS];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t soff = (int64_t)bh * N;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int col0 = rb * BC + wave_id() * 16 * MC;
+
+  u32x4 kf[MC][G::kChunks], vf[MC][G::kChunks];
+#pragma unroll
+  for (int mc = 0; mc < MC; ++mc) {
+    load_stationary<T, D>(kf[mc], K + hoff, col0 + 16 * mc + j, N);
+    load_stationary<T, D>(vf[mc], V + hoff, col0 + 16 * mc + j, N);
+  }
+  floatx4 dk[G::kNB][MC], dv[G::kNB][MC];
+#pragma unroll
+  for (int nb = 0; nb < G::kNB; ++nb)
+#pragma unroll
+    for (int mc = 0; mc < MC; ++mc) dk[nb][mc] = dv[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float c = scale * kLog2e;
+
+  TileCopy<T, D, NT, 2> cp;
+  const T* const src[2] = {Q + hoff, dO + hoff};
+  const float* const ssrc[2] = {L + soff, Dv + soff};
+  const int nT = (N + kBS - 1) / kBS;
+  cp.load(src, 0, N);
+  cp.store((T FB_LDS*)lds[0]);
+  copy_row_scalars<2>((float FB_LDS*)sc[0], ssrc, 0, N);
+  __syncthreads();
+  for (int it = 0; it < nT; ++it) {
+    const int s0 = it * kBS;
+    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* dOs = Qs + G::kTileElems;
+    const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
+    const float FB_LDS* Ds = Ls + kBS;
+
+    floatx4 s[2][MC], dp[2][MC];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int kk = 0; kk < G::kChunks; ++kk) {
+        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+        const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+          s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);
+          dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
+        }
+      }
+    typename E::TFrag pf[MC], dsf[MC];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+      const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ds + 16 * sb + 4 * g);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = s0 + 16 * sb + 4 * g + r < N;
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+          const float p = ok ? fast_exp2(s[sb][mc][r] * c - lv[r] * kLog2e) : 0.f;
+          pf[mc].set(4 * sb + r, p);
+          dsf[mc].set(4 * sb + r, p * (dp[sb][mc][r] - dv4[r]));
+        }
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < G::kNB; ++nb) {
+      const typename E::AFrag ado = E::load_afrag(dOs, G::kLdx, 16 * nb);
+      const typename E::AFrag aq = E::load_afrag(Qs, G::kLdx, 16 * nb);
+#pragma unroll
+      for (int mc = 0; mc < MC; ++mc) {
+        dv[nb][mc] = E::mma_acc(ado, pf[mc], dv[nb][mc]);
+        dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
+      }
+    }
+    if (it + 1 < nT) {
+      cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+      copy_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int mc = 0; mc < MC; ++mc) {
+    const int col = col0 + 16 * mc + j;
+    if (col < N) {
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) {
+        E::store4(dK + hoff + (int64_t)col * D + 16 * nb + 4 * g, dk[nb][mc] * scale);
+        E::store4(dV + hoff + (int64_t)col * D + 16 * nb + 4 * g, dv[nb][mc]);
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// BoB Pass 1 (row-major; Alg. 1/2 Pass 1 with the affine fusion of Prop. 3.1).
+// Stationary: Q, U_Q, dO rows (+ L, D).  Streamed: K, V, U_K, U_V.
+// Per tile it recomputes S, P, dP, F, C (as transposed tiles), forms
+// Pt0 = C + F (dP - D), and accumulates the six row accumulators
+//   alpha += rowsum(P F),  E0 += rowsum(P Pt0),
+//   dOt0 += P U_V + (P F) V,  Omega += (P Pt0) K + (P (dP - D)) U_K,
+//   Bacc += P K,  R += (P dP) K.
+// Epilogue (eq. 8): E = E0 - alpha D, dOt = dOt0 - alpha O,
+// Qt = tau (Omega - alpha R - E Bacc).  Writes alpha, E, Qt, dOt once.
+// ===========================================================================
+template <typename T, int D, int MR, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
+    const T* __restrict__ UK, const T* __restrict__ UV, const float* __restrict__ L,
+    const float* __restrict__ Dv, T* __restrict__ Qt, T* __restrict__ dOt,
+    float* __restrict__ alpha_out, float* __restrict__ E_out, int N, int nRB, int total, float scale) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NT = NW * 64;
+  constexpr int BR = 16 * MR * NW;
+  __shared__ __attribute__((aligned(16))) T lds[2][4 * G::kTileElems];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t soff = (int64_t)bh * N;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int row0 = rb * BR + wave_id() * 16 * MR;
+
+  u32x4 qf[MR][G::kChunks], uqf[MR][G::kChunks], dof[MR][G::kChunks];
+  float lb[MR], drow[MR];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    load_stationary<T, D>(qf[mb], Q + hoff, row, N);
+    load_stationary<T, D>(uqf[mb], UQ + hoff, row, N);
+    load_stationary<T, D>(dof[mb], dO + hoff, row, N);
+    lb[mb] = row < N ? L[soff + row] * kLog2e : 0.f;
+    drow[mb] = row < N ? Dv[soff + row] : 0.f;
+  }
+  floatx4 aDO[G::kNB][MR], aOM[G::kNB][MR], aB[G::kNB][MR], aR[G::kNB][MR];
+#pragma unroll
+  for (int nb = 0; nb < G::kNB; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb) aDO[nb][mb] = aOM[nb][mb] = aB[nb][mb] = aR[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float alpha[MR], e0[MR];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) alpha[mb] = e0[mb] = 0.f;
+  const float c = scale * kLog2e;
+
+  TileCopy<T, D, NT, 4> cp;
+  const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  cp.load(src, 0, N);
+  cp.store((T FB_LDS*)lds[0]);
+  __syncthreads();
+  for (int it = 0; it < nT; ++it) {
+    const int s0 = it * kBS;
+    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    const T FB_LDS* Ks = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* Vs = Ks + G::kTileElems;
+    const T FB_LDS* UKs = Vs + G::kTileElems;
+    const T FB_LDS* UVs = UKs + G::kTileElems;
+
+    // transposed score tiles: [s][t] = streamed . stationary
+    floatx4 s[2][MR], dp[2][MR], f[2][MR], cc[2][MR];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = f[sb][mb] = cc[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int kk = 0; kk < G::kChunks; ++kk) {
+        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const u32x4 ak = *(const u32x4 FB_LDS*)(Ks + off);
+        const u32x4 av = *(const u32x4 FB_LDS*)(Vs + off);
+        const u32x4 auk = *(const u32x4 FB_LDS*)(UKs + off);
+        const u32x4 auv = *(const u32x4 FB_LDS*)(UVs + off);
+#pragma unroll
+        for (int mb = 0; mb < MR; ++mb) {
+          s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);        // S^T = K Q^T
+          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);     // dP^T = V dO^T
+          f[sb][mb] = E::mma_chunk(ak, uqf[mb][kk], f[sb][mb]);       // (U_Q K^T)^T
+          f[sb][mb] = E::mma_chunk(auk, qf[mb][kk], f[sb][mb]);       // + (Q U_K^T)^T
+          cc[sb][mb] = E::mma_chunk(auv, dof[mb][kk], cc[sb][mb]);    // C^T = U_V dO^T
+        }
+      }
+    // elementwise: B-operand fragments for the accumulate step
+    typename E::TFrag fP[MR], fPF[MR], fPPt[MR], fPdd[MR], fPdp[MR];
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool ok = s0 + 16 * sb + 4 * g + r < N;
+          const float p = ok ? fast_exp2(s[sb][mb][r] * c - lb[mb]) : 0.f;
+          const float fv = f[sb][mb][r] * scale;
+          const float dpv = dp[sb][mb][r];
+          const float dd = dpv - drow[mb];
+          const float pt0 = __builtin_fmaf(fv, dd, cc[sb][mb][r]);
+          const float pf = p * fv;
+          const float ppt = p * pt0;
+          alpha[mb] += pf;
+          e0[mb] += ppt;
+          const int i = 4 * sb + r;
+          fP[mb].set(i, p);
+          fPF[mb].set(i, pf);
+          fPPt[mb].set(i, ppt);
+          fPdd[mb].set(i, p * dd);
+          fPdp[mb].set(i, p * dpv);
+        }
+    // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
+#pragma unroll
+    for (int nb = 0; nb < G::kNB; ++nb) {
+      const typename E::AFrag ak = E::load_afrag(Ks, G::kLdx, 16 * nb);
+      const typename E::AFrag av = E::load_afrag(Vs, G::kLdx, 16 * nb);
+      const typename E::AFrag auk = E::load_afrag(UKs, G::kLdx, 16 * nb);
+      const typename E::AFrag auv = E::load_afrag(UVs, G::kLdx, 16 * nb);
+#pragma unroll
+      for (int mb = 0; mb < MR; ++mb) {
+        aB[nb][mb] = E::mma_acc(ak, fP[mb], aB[nb][mb]);
+        aR[nb][mb] = E::mma_acc(ak, fPdp[mb], aR[nb][mb]);
+        aOM[nb][mb] = E::mma_acc(ak, fPPt[mb], aOM[nb][mb]);
+        aOM[nb][mb] = E::mma_acc(auk, fPdd[mb], aOM[nb][mb]);
+        aDO[nb][mb] = E::mma_acc(auv, fP[mb], aDO[nb][mb]);
+        aDO[nb][mb] = E::mma_acc(av, fPF[mb], aDO[nb][mb]);
+      }
+    }
+    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    __syncthreads();
+  }
+  // epilogue (eq. 8)
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    const float al = group_sum(alpha[mb]);
+    const float ee = group_sum(e0[mb]) - al * drow[mb];
+    if (row < N) {
+      if (g == 0) {
+        alpha_out[soff + row] = al;
+        E_out[soff + row] = ee;
+      }
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) {
+        const int64_t off = hoff + (int64_t)row * D + 16 * nb + 4 * g;
+        const floatx4 o = E::load4(O + off);
+        E::store4(dOt + off, aDO[nb][mb] - al * o);
+        E::store4(Qt + off, scale * (aOM[nb][mb] - al * aR[nb][mb] - ee * aB[nb][mb]));
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// BoB Pass 2 (column-major; Alg. 1/2 Pass 2).  Stationary: K, V, U_K, U_V
+// rows.  Streamed: Q, U_Q, dO tiles with L, D, alpha, E.  Per tile:
+//   h = F - alpha, dS = P (dP - D), Pt = C + F (dP - D) - alpha dP,
+//   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
+// Writes Kt, Vt once; no atomics.
+// ===========================================================================
+template <typename T, int D, int MC, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
+    const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
+    const float* __restrict__ alpha_in, const float* __restrict__ E_in,
+    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NT = NW * 64;
+  constexpr int BC = 16 * MC * NW;
+  __shared__ __attribute__((aligned(16))) T lds[2][3 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) float sc[2][4 * kBS];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t soff = (int64_t)bh * N;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int col0 = rb * BC + wave_id() * 16 * MC;
+
+  u32x4 kf[MC][G::kChunks], vf[MC][G::kChunks], ukf[MC][G::kChunks], uvf[MC][G::kChunks];
+#pragma unroll
+  for (int mc = 0; mc < MC; ++mc) {
+    const int col = col0 + 16 * mc + j;
+    load_stationary<T, D>(kf[mc], K + hoff, col, N);
+    load_stationary<T, D>(vf[mc], V + hoff, col, N);
+    load_stationary<T, D>(ukf[mc], UK + hoff, col, N);
+    load_stationary<T, D>(uvf[mc], UV + hoff, col, N);
+  }
+  floatx4 aK[G::kNB][MC], aV[G::kNB][MC];
+#pragma unroll
+  for (int nb = 0; nb < G::kNB; ++nb)
+#pragma unroll
+    for (int mc = 0; mc < MC; ++mc) aK[nb][mc] = aV[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const float c = scale * kLog2e;
+
+  TileCopy<T, D, NT, 3> cp;
+  const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
+  const float* const ssrc[4] = {L + soff, Dv + soff, alpha_in + soff, E_in + soff};
+  const int nT = (N + kBS - 1) / kBS;
+  cp.load(src, 0, N);
+  cp.store((T FB_LDS*)lds[0]);
+  copy_row_scalars<4>((float FB_LDS*)sc[0], ssrc, 0, N);
+  __syncthreads();
+  for (int it = 0; it < nT; ++it) {
+    const int s0 = it * kBS;
+    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* UQs = Qs + G::kTileElems;
+    const T FB_LDS* dOs = UQs + G::kTileElems;
+    const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
+
+    // score tiles [s = query][t = key]
+    floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = f[sb][mc] = cc[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int kk = 0; kk < G::kChunks; ++kk) {
+        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+        const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
+        const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+          s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
+          dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP = dO V^T
+          f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // U_Q K^T
+          f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       // + Q U_K^T
+          cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C = dO U_V^T
+        }
+      }
+    typename E::TFrag fPh[MC], fSt[MC], fdS[MC];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+      const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ls + kBS + 16 * sb + 4 * g);
+      const floatx4 av4 = *(const floatx4 FB_LDS*)(Ls + 2 * kBS + 16 * sb + 4 * g);
+      const floatx4 ev4 = *(const floatx4 FB_LDS*)(Ls + 3 * kBS + 16 * sb + 4 * g);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = s0 + 16 * sb + 4 * g + r < N;
+#pragma unroll
+        for (int mc = 0; mc < MC; ++mc) {
+          const float p = ok ? fast_exp2(s[sb][mc][r] * c - lv[r] * kLog2e) : 0.f;
+          const float fv = f[sb][mc][r] * scale;
+          const float dpv = dp[sb][mc][r];
+          const float dd = dpv - dv4[r];
+          const float pt = __builtin_fmaf(fv, dd, cc[sb][mc][r]) - av4[r] * dpv;
+          const int i = 4 * sb + r;
+          fPh[mc].set(i, p * (fv - av4[r]));
+          fSt[mc].set(i, p * (pt - ev4[r]));
+          fdS[mc].set(i, p * dd);
+        }
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < G::kNB; ++nb) {
+      const typename E::AFrag aq = E::load_afrag(Qs, G::kLdx, 16 * nb);
+      const typename E::AFrag auq = E::load_afrag(UQs, G::kLdx, 16 * nb);
+      const typename E::AFrag ado = E::load_afrag(dOs, G::kLdx, 16 * nb);
+#pragma unroll
+      for (int mc = 0; mc < MC; ++mc) {
+        aV[nb][mc] = E::mma_acc(ado, fPh[mc], aV[nb][mc]);
+        aK[nb][mc] = E::mma_acc(aq, fSt[mc], aK[nb][mc]);
+        aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
+      }
+    }
+    if (it + 1 < nT) {
+      cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+      copy_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int mc = 0; mc < MC; ++mc) {
+    const int col = col0 + 16 * mc + j;
+    if (col < N) {
+#pragma unroll
+      for (int nb = 0; nb < G::kNB; ++nb) {
+        const int64_t off = hoff + (int64_t)col * D + 16 * nb + 4 * g;
+        E::store4(Kt + off, aK[nb][mc] * scale);
+        E::store4(Vt + off, aV[nb][mc]);
+      }
+    }
+  }
+}
+
+}  // namespace fb

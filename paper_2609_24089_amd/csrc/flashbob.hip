@@ -1,0 +1,218 @@
+// C ABI of libflashbob.so: argument validation and kernel dispatch.
+// The entry points are declared (and documented) in include/flashbob.h.
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/flashbob.h"
+#include "fb_kernels.h"
+
+namespace fb {
+namespace {
+
+// Launch shapes per (element type, head dim): MR/MC = 16-row MFMA blocks per
+// wave, NW = waves per workgroup.  A workgroup owns 16*MR*NW stationary rows.
+template <typename T, int D> struct Cfg;
+template <> struct Cfg<bf16, 64> {
+  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 2, kP2MC = 2;
+};
+template <> struct Cfg<bf16, 128> {
+  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 1, kP2MC = 1;
+};
+template <> struct Cfg<float, 64> {
+  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1;
+};
+template <> struct Cfg<float, 128> {
+  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1;
+};
+
+constexpr int64_t kMaxN = int64_t(1) << 30;
+
+bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Problem {
+  int32_t dtype;
+  int64_t B, H, N, d;
+  float scale;
+};
+
+// Returns BOB_OK to proceed, or an error; sets *empty for B*H*N == 0.
+int32_t check_problem(const Problem& p, bool* empty) {
+  *empty = false;
+  if (p.dtype != BOB_F32 && p.dtype != BOB_BF16) return BOB_EINVAL;
+  if (p.B < 0 || p.H < 0 || p.N < 0 || p.d < 1) return BOB_EINVAL;
+  if (!std::isfinite(p.scale)) return BOB_EINVAL;
+  if (p.d != 64 && p.d != 128) return BOB_EUNSUPPORTED;
+  if (p.B == 0 || p.H == 0 || p.N == 0) {
+    *empty = true;
+    return BOB_OK;
+  }
+  if (p.N > kMaxN) return BOB_EINVAL;
+  // grid size: heads x row blocks must fit a 32-bit grid (smallest block is 64 rows)
+  const int64_t heads = p.B * p.H;
+  if (p.B > INT32_MAX || p.H > INT32_MAX || heads > INT32_MAX) return BOB_EINVAL;
+  if (heads * ((p.N + 63) / 64) > INT32_MAX) return BOB_EINVAL;
+  return BOB_OK;
+}
+
+int32_t check_ptrs(std::initializer_list<const void*> ptrs) {
+  for (const void* q : ptrs)
+    if (!aligned16(q)) return BOB_EINVAL;
+  return BOB_OK;
+}
+
+int32_t finish_launch() { return hipGetLastError() == hipSuccess ? BOB_OK : BOB_ELAUNCH; }
+
+struct Grid {
+  int nRB, total;
+};
+Grid grid_for(const Problem& p, int rows_per_block) {
+  Grid g;
+  g.nRB = (int)((p.N + rows_per_block - 1) / rows_per_block);
+  g.total = (int)(p.B * p.H * g.nRB);
+  return g;
+}
+
+template <typename T, int D>
+int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V, void* O, float* L,
+                   hipStream_t s) {
+  using C = Cfg<T, D>;
+  const Grid g = grid_for(p, 16 * C::kFwdMR * C::kNW);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((attn_fwd_kernel<T, D, C::kFwdMR, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale);
+  return finish_launch();
+}
+
+template <typename T, int D>
+int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
+                   const void* dO, const float* L, void* dQ, void* dK, void* dV, float* Dv,
+                   hipStream_t s) {
+  using C = Cfg<T, D>;
+  const Grid gr = grid_for(p, 16 * C::kRowsMR * C::kNW);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, C::kRowsMR, C::kNW>), dim3(gr.total), dim3(64 * C::kNW), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, L, (T*)dQ, Dv,
+                     (int)p.N, gr.nRB, gr.total, p.scale);
+  int32_t rc = finish_launch();
+  if (rc != BOB_OK) return rc;
+  const Grid gc = grid_for(p, 16 * C::kColsMC * C::kNW);
+  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, C::kColsMC, C::kNW>), dim3(gc.total), dim3(64 * C::kNW), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
+                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale);
+  return finish_launch();
+}
+
+template <typename T, int D>
+int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
+                     const void* dO, const void* UQ, const void* UK, const void* UV, const float* L,
+                     const float* Dv, void* Qt, void* dOt, float* alpha, float* E, hipStream_t s) {
+  using C = Cfg<T, D>;
+  const Grid g = grid_for(p, 16 * C::kP1MR * C::kNW);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, (const T*)UQ,
+                     (const T*)UK, (const T*)UV, L, Dv, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB,
+                     g.total, p.scale);
+  return finish_launch();
+}
+
+template <typename T, int D>
+int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
+                     const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
+                     const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s) {
+  using C = Cfg<T, D>;
+  const Grid g = grid_for(p, 16 * C::kP2MC * C::kNW);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((bob_pass2_kernel<T, D, C::kP2MC, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
+                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale);
+  return finish_launch();
+}
+
+// Dispatch on (dtype, d) to a templated launcher.
+#define FB_DISPATCH(p, FN, ...)                                                  \
+  do {                                                                           \
+    if ((p).dtype == BOB_BF16 && (p).d == 64) return FN<fb::bf16, 64>(__VA_ARGS__);  \
+    if ((p).dtype == BOB_BF16 && (p).d == 128) return FN<fb::bf16, 128>(__VA_ARGS__); \
+    if ((p).dtype == BOB_F32 && (p).d == 64) return FN<float, 64>(__VA_ARGS__);  \
+    if ((p).dtype == BOB_F32 && (p).d == 128) return FN<float, 128>(__VA_ARGS__); \
+    return BOB_EUNSUPPORTED;                                                     \
+  } while (0)
+
+}  // namespace
+}  // namespace fb
+
+using fb::Problem;
+
+extern "C" {
+
+int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                     const void* Q, const void* K, const void* V, void* O, float* L, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, L});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_fwd, p, Q, K, V, O, L, (hipStream_t)stream);
+}
+
+int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                 const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream);
+}
+
+int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                            const void* Q, const void* K, const void* V, const void* O,
+                            const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                            const float* L, const float* D, void* Qt, void* dOt, float* alpha,
+                            float* E, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, dO, gdQ, gdK, gdV, L, D, Qt, dOt, alpha, E});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_pass1, p, Q, K, V, O, dO, gdQ, gdK, gdV, L, D, Qt, dOt, alpha, E,
+              (hipStream_t)stream);
+}
+
+int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                            const void* Q, const void* K, const void* V, const void* dO,
+                            const void* gdQ, const void* gdK, const void* gdV, const float* L,
+                            const float* D, const float* alpha, const float* E, void* Kt, void* Vt,
+                            void* stream) {
+  const Problem p{dtype, B, H, N, d, scale};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
+              (hipStream_t)stream);
+}
+
+int32_t bob_supported(int32_t dtype, int64_t d) {
+  return (dtype == BOB_F32 || dtype == BOB_BF16) && (d == 64 || d == 128) ? 1 : 0;
+}
+
+const char* bob_status_string(int32_t status) {
+  switch (status) {
+    case BOB_OK: return "BOB_OK: success";
+    case BOB_EINVAL: return "BOB_EINVAL: invalid argument (size, scale, dtype, or NULL/misaligned pointer)";
+    case BOB_EUNSUPPORTED: return "BOB_EUNSUPPORTED: (dtype, head dim) not built; supported d = 64, 128";
+    case BOB_ELAUNCH: return "BOB_ELAUNCH: HIP kernel launch failed";
+    default: return "unknown bob_status";
+  }
+}
+
+const char* bob_version(void) { return "flashbob-gfx950 0.1"; }
+
+}  // extern "C"

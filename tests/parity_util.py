@@ -1,0 +1,44 @@
+"""Helpers shared by the GPU parity tests (test-side only)."""
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from workloads import NAMES, as_f64
+
+# Normwise relative error bars: ||x - y||_F / ||y||_F per output tensor.
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def lib():
+    import paper_2609_24089_amd as fb
+    fb.load_library()
+    return fb
+
+
+def to_dev(x):
+    return {k: v.cuda() for k, v in x.items()}
+
+
+def nrel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def oracle_full(x, scale):
+    args = [as_f64(x[n]) for n in NAMES]
+    return oracle.bob(*args, scale)
+
+
+def run_gpu_path(xd, scale):
+    fb = lib()
+    out = fb.bob(*[xd[n] for n in NAMES], scale)
+    torch.cuda.synchronize()
+    return out

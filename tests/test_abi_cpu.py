@@ -1,0 +1,107 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+include/flashbob.h declares, and rejects bad arguments with the documented
+status codes before any HIP call is made (so nothing here touches a device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_24089_amd as fb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashbob.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fb.LIB_PATH):
+        from paper_2609_24089_amd.build import build_library
+        build_library()
+    return fb.load_library()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols",
+              "bob_supported", "bob_status_string", "bob_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_supported_and_strings(lib):
+    assert lib.bob_supported(fb.BOB_BF16, 64) == 1 and lib.bob_supported(fb.BOB_BF16, 128) == 1
+    assert lib.bob_supported(fb.BOB_F32, 64) == 1 and lib.bob_supported(fb.BOB_F32, 128) == 1
+    assert lib.bob_supported(fb.BOB_BF16, 96) == 0 and lib.bob_supported(7, 64) == 0
+    for rc in range(4):
+        assert lib.bob_status_string(rc).decode().startswith("BOB_")
+    assert lib.bob_status_string(99).decode() == "unknown bob_status"
+    assert lib.bob_version().decode().startswith("flashbob")
+
+
+ALIGNED = 1 << 20          # fake, 16-byte aligned addresses: never dereferenced
+MISALIGNED = (1 << 20) + 8
+
+
+def call(lib, fn, dtype=fb.BOB_BF16, B=1, H=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None):
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 14, "attn_bob_pass2_cols": 13}[fn]
+    ptrs = [ctypes.c_void_p(ptr) for _ in range(nptr)]
+    if bad_index is not None:
+        ptrs[bad_index] = ctypes.c_void_p(0)
+    return getattr(lib, fn)(dtype, B, H, N, d, ctypes.c_float(scale), *ptrs, None)
+
+
+FNS = ["attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"]
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_rejects_bad_arguments_without_launching(lib, fn):
+    assert call(lib, fn, N=-1) == fb.BOB_EINVAL
+    assert call(lib, fn, B=-2) == fb.BOB_EINVAL
+    assert call(lib, fn, H=-1) == fb.BOB_EINVAL
+    assert call(lib, fn, d=0) == fb.BOB_EINVAL
+    assert call(lib, fn, scale=float("nan")) == fb.BOB_EINVAL
+    assert call(lib, fn, scale=float("inf")) == fb.BOB_EINVAL
+    assert call(lib, fn, dtype=5) == fb.BOB_EINVAL
+    assert call(lib, fn, d=96) == fb.BOB_EUNSUPPORTED
+    assert call(lib, fn, d=32) == fb.BOB_EUNSUPPORTED
+    assert call(lib, fn, ptr=MISALIGNED) == fb.BOB_EINVAL
+    assert call(lib, fn, ptr=0) == fb.BOB_EINVAL
+    assert call(lib, fn, N=(1 << 30) + 1) == fb.BOB_EINVAL
+    assert call(lib, fn, B=1 << 20, H=1 << 20) == fb.BOB_EINVAL
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_every_pointer_is_checked(lib, fn):
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 14, "attn_bob_pass2_cols": 13}[fn]
+    for i in range(nptr):
+        assert call(lib, fn, bad_index=i) == fb.BOB_EINVAL, i
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_empty_problem_is_a_no_op(lib, fn):
+    # B*H*N == 0 touches no memory, so NULL pointers are fine
+    assert call(lib, fn, N=0, ptr=0) == fb.BOB_OK
+    assert call(lib, fn, B=0, ptr=0) == fb.BOB_OK
+    assert call(lib, fn, H=0, d=128, ptr=0) == fb.BOB_OK
+    # an unsupported head dim is reported even for an empty problem
+    assert call(lib, fn, N=0, d=80, ptr=0) == fb.BOB_EUNSUPPORTED
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        fb.attn_fwd_lse(x, x, x, 0.125)
+    with pytest.raises(TypeError):
+        fb._dtype_code(torch.zeros(1, dtype=torch.float16))
