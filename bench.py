@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Throughput of exact attention backward-over-backward (BoB) on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic
+inputs already resident in HBM: attn_fwd_lse -> attn_bwd -> BoB Pass 1 ->
+BoB Pass 2, all on one stream.  The headline `value` is BoB TFLOP/s:
+38*B*H*N^2*d executed MFMA FLOPs (Pass 1 does 11 and Pass 2 does 8 tile
+contractions of 2*N^2*d each) divided by the time of Pass 1 + Pass 2,
+measured with HIP events around the two passes inside every timed step
+(median over steps).  `ms_per_step` is the wall time of the whole step.
+
+Prints ONE JSON line.  Default workload: B=1, H=16, N=16384, d=128, bf16
+(Q, K ~ 0.5*N(0,1), the rest N(0,1), seed 2).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published dense peaks (TFLOP/s): bf16 MFMA 2.5 PFLOP/s class
+# (256 CUs x 2.4 GHz x 4096 FLOP/clk/CU = 2516.6), fp32 157.3.
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+# executed MFMA FLOPs per (b, h) in units of N^2 * d, per library call
+FLOP_COEF = {"fwd": 4, "bwd": 14, "pass1": 22, "pass2": 16}
+
+KERNEL_SOURCES = ["fb_common.h", "fb_kernels.h", "flashbob.hip"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_24089_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if there is none for this kernel/workload or the sources changed."""
+    try:
+        doc = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if doc.get("source_hash") != kernel_source_hash():
+        return None
+    ent = doc.get("kernels", {}).get(kernel, {})
+    if ent.get("workload") != workload:
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
+    """Time the float64 oracle (as it stands) on a bounded sample of the same
+    workload: the row-owned BoB outputs (Qt, dOt, alpha, E) of consecutive
+    `slab`-row query slabs, head after head, until about `budget_s` seconds of
+    CPU work are done.  Rate = Pass-1 executed FLOPs of those rows
+    (22 * rows * N * d) / time."""
+    import numpy as np
+    from oracle import bob_rows
+    from workloads import NAMES, as_f64
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    slab = min(slab, w.N)
+    rows, dt, heads_used = 0, 0.0, 0
+    for b in range(w.B):
+        for h in range(w.H):
+            mats = [as_f64(x_cpu[n][b, h]) for n in NAMES]
+            heads_used += 1
+            for r0 in range(0, w.N, slab):
+                sel = np.arange(r0, min(w.N, r0 + slab))
+                t0 = time.perf_counter()
+                bob_rows(*mats, w.scale, sel)
+                dt += time.perf_counter() - t0
+                rows += len(sel)
+                if dt >= budget_s:
+                    break
+            if dt >= budget_s:
+                break
+        if dt >= budget_s:
+            break
+    flops = 22.0 * rows * w.N * w.d
+    return {
+        "value": round(flops / dt / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"float64 oracle bob_rows on {rows} query rows ({slab}-row slabs over {heads_used} "
+                   f"head(s)) of {w.name}: row-owned outputs Qt, dOt, alpha, E in {dt:.1f} s; rate counts "
+                   f"the Pass-1 FLOPs 22*rows*N*d; BLAS threads={threads}, host cores={os.cpu_count()}"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="bf16_b1h16_n16384_d128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run one device-to-device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "gpus_requested": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2609_24089_amd as fb
+    from workloads import WORKLOADS, workload_inputs
+
+    log = lambda msg: print(f"[bench] {msg}", file=sys.stderr, flush=True)
+    fb.load_library()
+    w = WORKLOADS[args.workload]
+    log(f"workload {w.name}: generating inputs")
+    x_cpu = workload_inputs(w)
+    dev = torch.device("cuda:0")
+    x = {k: v.to(dev) for k, v in x_cpu.items()}
+    Q, K, V, dO, UQ, UK, UV = (x[n] for n in ("Q", "K", "V", "dO", "UQ", "UK", "UV"))
+    rows_shape = (w.B, w.H, w.N)
+    E_ = lambda: torch.empty_like(Q)
+    R_ = lambda: torch.empty(rows_shape, dtype=torch.float32, device=dev)
+    O, L = E_(), R_()
+    dQ, dK, dV, Dv = E_(), E_(), E_(), R_()
+    Qt, dOt, alpha, Eb = E_(), E_(), R_(), R_()
+    Kt, Vt = E_(), E_()
+    s = w.scale
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * 2**20 // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
+        log(f"copy calibration: {args.copy_calibration_mib} MiB read + written")
+
+    def step(ev):
+        ev[0].record()
+        fb.attn_fwd_lse(Q, K, V, s, out=(O, L))
+        ev[1].record()
+        fb.attn_bwd(Q, K, V, O, dO, L, s, out=(dQ, dK, dV, Dv))
+        ev[2].record()
+        fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, Dv, s, out=(Qt, dOt, alpha, Eb))
+        ev[3].record()
+        fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, Dv, alpha, Eb, s, out=(Kt, Vt))
+        ev[4].record()
+
+    mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    torch.cuda.reset_peak_memory_stats(dev)
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step(mk())
+    events = [mk() for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    log(f"timed {args.steps} steps in {wall:.2f} s")
+
+    names = ("fwd", "bwd", "pass1", "pass2")
+    per = {n: [ev[i].elapsed_time(ev[i + 1]) for ev in events] for i, n in enumerate(names)}
+    bob_ms = sorted(a + b for a, b in zip(per["pass1"], per["pass2"]))
+    q = lambda xs, f: xs[min(len(xs) - 1, int(f * len(xs)))]
+    bob_med = statistics.median(bob_ms)
+    unit = w.B * w.H * float(w.N) ** 2 * w.d
+    peak = PEAK_TFLOPS[w.dtype]
+    value = 38.0 * unit / (bob_med * 1e-3) / 1e12
+    kern = {}
+    for n in names:
+        mean_ms = statistics.mean(per[n])
+        tf = FLOP_COEF[n] * unit / (mean_ms * 1e-3) / 1e12
+        kern[n] = {"ms_mean": round(mean_ms, 4), "ms_median": round(statistics.median(per[n]), 4),
+                   "tflops": round(tf, 2), "frac_peak": round(tf / peak, 4)}
+    dom = max(("pass1", "pass2"), key=lambda n: statistics.mean(per[n]))
+    dom_ms = statistics.mean(per[dom])
+    achieved = FLOP_COEF[dom] * unit / (dom_ms * 1e-3) / 1e12
+    traffic = measured_traffic(dom, w.name)
+    step_flops = sum(FLOP_COEF.values()) * unit
+
+    line = {
+        "metric": "BoB TFLOP/s (38*B*H*N^2*d / time of Pass 1 + Pass 2) and % of MI355X dense bf16 MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "scale": w.scale,
+                   "seed": w.seed, "qk_scale": w.qk_scale, "causal": False},
+        "pct_peak": round(100.0 * value / peak, 2),
+        "bob_ms": {"median": round(bob_med, 4), "p20": round(q(bob_ms, 0.2), 4),
+                   "p80": round(q(bob_ms, 0.8), 4)},
+        "bob_tflops_min_count": round(24.0 * unit / (bob_med * 1e-3) / 1e12, 2),
+        "step_tflops": round(step_flops / (wall / args.steps) / 1e12, 2),
+        "kernels": kern,
+        "peak_mem_gib": round(torch.cuda.max_memory_allocated(dev) / 2**30, 3),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle for about {args.cpu_seconds} s")
+        line["cpu_baseline"] = cpu_baseline(x_cpu, w, budget_s=args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -100,23 +100,29 @@ def _rows_empty(shape, like):
     return torch.empty(tuple(shape[:3]), dtype=torch.float32, device=like.device)
 
 
-def attn_fwd_lse(Q, K, V, scale, stream=None):
+def attn_fwd_lse(Q, K, V, scale, out=None, stream=None):
     """Forward attention (eq. 1): returns (O, L)."""
     B, H, N, d = _check_mats(Q, K, V)
-    O = torch.empty_like(Q)
-    L = _rows_empty(Q.shape, Q)
+    if out is None:
+        out = (torch.empty_like(Q), _rows_empty(Q.shape, Q))
+    O, L = out
+    _check_mats(Q, O)
+    _check_rows(Q.shape, L)
     lib = load_library()
     _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale),
           _p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
     return O, L
 
 
-def attn_bwd(Q, K, V, O, dO, L, scale, stream=None):
+def attn_bwd(Q, K, V, O, dO, L, scale, out=None, stream=None):
     """First backward (eqs. 2-3): returns (dQ, dK, dV, D)."""
     B, H, N, d = _check_mats(Q, K, V, O, dO)
     _check_rows(Q.shape, L)
-    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q)
-    D = _rows_empty(Q.shape, Q)
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q))
+    dQ, dK, dV, D = out
+    _check_mats(Q, dQ, dK, dV)
+    _check_rows(Q.shape, D)
     lib = load_library()
     _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale),
           _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
@@ -130,6 +136,8 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, out=None, st
     if out is None:
         out = (torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q), _rows_empty(Q.shape, Q))
     Qt, dOt, alpha, E = out
+    _check_mats(Q, Qt, dOt)
+    _check_rows(Q.shape, alpha, E)
     lib = load_library()
     _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale),
           _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
@@ -144,6 +152,7 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, out=N
     if out is None:
         out = (torch.empty_like(Q), torch.empty_like(Q))
     Kt, Vt = out
+    _check_mats(Q, Kt, Vt)
     lib = load_library()
     _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale),
           _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
@@ -157,8 +166,8 @@ def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, stream=None):
     Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
     O, L, D, dQ, dK, dV.
     """
-    O, L = attn_fwd_lse(Q, K, V, scale, stream)
-    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, stream)
+    O, L = attn_fwd_lse(Q, K, V, scale, stream=stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, stream=stream)
     Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, stream=stream)
     Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, stream=stream)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)
