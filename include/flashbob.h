@@ -78,13 +78,18 @@ int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, floa
 
 /* BoB Pass 1, row-major (Alg. 1 Pass 1; Prop. 3.1 and eq. 8).
  * In:  Q, K, V, O, dO, gdQ (= U_Q), gdK (= U_K), gdV (= U_V) [B,H,N,d];
- *      L, D fp32 [B,H,N] from attn_fwd_lse / attn_bwd.
+ *      L, D fp32 [B,H,N] from attn_fwd_lse / attn_bwd;
+ *      dQ [B,H,N,d] from attn_bwd, OPTIONAL (may be NULL).
  * Out: Qt, dOt [B,H,N,d];  alpha, E fp32 [B,H,N] -- the two row scalars
- *      alpha_i = sum_j P_ij F_ij and E_i = sum_j P_ij Pt_ij that Pass 2 reads. */
+ *      alpha_i = sum_j P_ij F_ij and E_i = sum_j P_ij Pt_ij that Pass 2 reads.
+ * With dQ == NULL the kernel keeps the six row accumulators of Prop. 3.1.
+ * With dQ given it drops R = sum_j P_ij dP_ij k_j, using R = dQ/scale + D B
+ * (so Qt = scale (Omega - E0 B) - alpha dQ, E0 = E + alpha D); the result is
+ * the same up to rounding and the d = 128 kernel fits two waves per SIMD. */
 int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
                             const void* Q, const void* K, const void* V, const void* O,
                             const void* dO, const void* gdQ, const void* gdK, const void* gdV,
-                            const float* L, const float* D,
+                            const float* L, const float* D, const void* dQ,
                             void* Qt, void* dOt, float* alpha, float* E, void* stream);
 
 /* BoB Pass 2, column-major (Alg. 1 Pass 2).

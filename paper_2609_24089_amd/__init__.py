@@ -35,7 +35,7 @@ def load_library():
     common = [i32, i64, i64, i64, i64, f32]
     lib.attn_fwd_lse.argtypes = common + [vp] * 5 + [vp]
     lib.attn_bwd.argtypes = common + [vp] * 10 + [vp]
-    lib.attn_bob_pass1_rows.argtypes = common + [vp] * 14 + [vp]
+    lib.attn_bob_pass1_rows.argtypes = common + [vp] * 15 + [vp]
     lib.attn_bob_pass2_cols.argtypes = common + [vp] * 13 + [vp]
     for fn in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"):
         getattr(lib, fn).restype = i32
@@ -129,9 +129,14 @@ def attn_bwd(Q, K, V, O, dO, L, scale, out=None, stream=None):
     return dQ, dK, dV, D
 
 
-def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, out=None, stream=None):
-    """BoB Pass 1 (row-major): returns (Qt, dOt, alpha, E)."""
+def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, dQ=None, out=None, stream=None):
+    """BoB Pass 1 (row-major): returns (Qt, dOt, alpha, E).
+
+    dQ (the first-backward output) is optional; when given, the kernel uses
+    it in place of the R accumulator (see include/flashbob.h)."""
     B, H, N, d = _check_mats(Q, K, V, O, dO, gdQ, gdK, gdV)
+    if dQ is not None:
+        _check_mats(Q, dQ)
     _check_rows(Q.shape, L, D)
     if out is None:
         out = (torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q), _rows_empty(Q.shape, Q))
@@ -141,7 +146,7 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, out=None, st
     lib = load_library()
     _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale),
           _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
-          _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
+          None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
     return Qt, dOt, alpha, E
 
 
@@ -160,14 +165,18 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, out=N
     return Kt, Vt
 
 
-def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, stream=None):
+def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, use_dq=True, stream=None):
     """Whole path: forward, first backward, Pass 1, Pass 2 on one stream.
+
+    use_dq=True hands the first-backward dQ to Pass 1 (five-accumulator form);
+    use_dq=False runs the six-accumulator form of Prop. 3.1.
 
     Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
     O, L, D, dQ, dK, dV.
     """
     O, L = attn_fwd_lse(Q, K, V, scale, stream=stream)
     dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, stream=stream)
-    Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, stream=stream)
+    Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale,
+                                            dQ=dQ if use_dq else None, stream=stream)
     Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, stream=stream)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)

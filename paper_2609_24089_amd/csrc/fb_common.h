@@ -83,15 +83,6 @@ template <> struct Elt<bf16> {
     bf16x8 v;
     __device__ __forceinline__ void set(int i, float x) { v[i] = (bf16)x; }
   };
-  static __device__ __forceinline__ AFrag load_afrag(const bf16 FB_LDS* X, int ldx, int dim0) {
-    const int l = lane_id(), g = l >> 4, j = l & 15;
-    const bf16 FB_LDS* p = X + (4 * g + (j >> 2)) * ldx + dim0 + 4 * (j & 3);
-    shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)p);
-    shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)(p + 16 * ldx));
-    AFrag a;
-    a.v = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    return a;
-  }
   static __device__ __forceinline__ floatx4 mma_acc(const AFrag& a, const TFrag& b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
   }
@@ -135,15 +126,6 @@ template <> struct Elt<float> {
     float v[8];
     __device__ __forceinline__ void set(int i, float x) { v[i] = x; }
   };
-  static __device__ __forceinline__ AFrag load_afrag(const float FB_LDS* X, int ldx, int dim0) {
-    const int l = lane_id(), g = l >> 4, j = l & 15;
-    AFrag a;
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) a.v[4 * h + r] = X[(16 * h + 4 * g + r) * ldx + dim0 + j];
-    return a;
-  }
   static __device__ __forceinline__ floatx4 mma_acc(const AFrag& a, const TFrag& b, floatx4 c) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[i], b.v[i], c, 0, 0, 0);
@@ -158,16 +140,65 @@ template <> struct Elt<float> {
 };
 
 // ---------------------------------------------------------------------------
-// Geometry helpers
+// LDS tile geometry.  A streamed tile is kBS rows x D elements, stored
+// without padding; the 16-byte chunks of row r are permuted by XOR with
+// swz(r) so that both access patterns are free of bank conflicts:
+//   * score A-operand reads (ds_read_b128): 16 lanes read one chunk from each
+//     of 16 consecutive rows -> swz must be a bijection on those rows;
+//   * transposed reads (ds_read_b64_tr_b16, bf16 only): 32 lanes read a
+//     32-byte chunk pair from each of 8 consecutive rows -> the pair index
+//     (c ^ swz(r)) >> 1 must differ across those rows.
+// fp32 tiles use swz(r) = r mod 16 (their accumulate operands are scalar
+// reads of one 64-byte run per row, which that also spreads).
 // ---------------------------------------------------------------------------
 template <typename T, int D> struct Geo {
-  static constexpr int kChunks = D * (int)sizeof(T) / 64;       // score chunks per row (per lane group)
   static constexpr int kCPR = D * (int)sizeof(T) / 16;          // 16-byte chunks per row
-  static constexpr int kPad = 16 / (int)sizeof(T);              // +16 bytes per LDS row
-  static constexpr int kLdx = D + kPad;                          // LDS row stride (elements)
-  static constexpr int kTileElems = kBS * kLdx;                  // one streamed tile in LDS
+  static constexpr int kChunks = D * (int)sizeof(T) / 64;       // score MFMA steps per row
+  static constexpr int kEPC = 16 / (int)sizeof(T);              // elements per chunk
+  static constexpr int kTileElems = kBS * D;                     // one streamed tile in LDS
   static constexpr int kNB = D / 16;                             // 16-dim output blocks
-  static __device__ __forceinline__ int chunk_elem(int kk, int g) { return kk * Elt<T>::kKC + g * (Elt<T>::kKC / 4); }
+  static constexpr int kBlocks = kBS * kCPR / 64;                // 1 KB blocks per tile
+
+  static __device__ __forceinline__ int swz(int r) {
+    if constexpr (sizeof(T) == 4) {
+      return r & 15;
+    } else if constexpr (D == 128) {
+      return ((r & 7) << 1) | ((r >> 3) & 1);
+    } else {
+      static_assert(D == 64, "head dim");
+      return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+    }
+  }
+  // element offset of logical chunk c of tile row r
+  static __device__ __forceinline__ int chunk_off(int r, int c) { return r * D + ((c ^ swz(r)) * kEPC); }
+
+  // score A-operand: row r, the lane group's chunk of MFMA step kk
+  static __device__ __forceinline__ u32x4 read_chunk(const T FB_LDS* X, int r, int kk) {
+    return *(const u32x4 FB_LDS*)(X + chunk_off(r, 4 * kk + (lane_id() >> 4)));
+  }
+
+  // A-operand of the accumulate step: dims [dim0, dim0+16) x the 32 tile rows,
+  // transposed; lane l gets rows {4g..4g+3, 16+4g..16+4g+3} (g = l >> 4) of
+  // dim dim0 + (l & 15), matching the score tiles' row order.
+  static __device__ __forceinline__ typename Elt<T>::AFrag load_afrag(const T FB_LDS* X, int dim0) {
+    const int l = lane_id(), g = l >> 4, j = l & 15;
+    typename Elt<T>::AFrag a;
+    if constexpr (sizeof(T) == 2) {
+      const int r = 4 * g + (j >> 2);
+      const int c = (dim0 >> 3) + ((j & 3) >> 1);
+      const int sub = 4 * (j & 1);
+      shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)(X + chunk_off(r, c) + sub));
+      shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((shortx4 FB_LDS*)(X + chunk_off(r + 16, c) + sub));
+      a.v = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    } else {
+      const int dim = dim0 + j;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) a.v[4 * h + r] = X[chunk_off(16 * h + 4 * g + r, dim >> 2) + (dim & 3)];
+    }
+    return a;
+  }
 };
 
 // Map a workgroup to (head, row block).  Workgroups are dispatched round-robin
@@ -181,7 +212,8 @@ __device__ __forceinline__ void map_block(int nRB, int total, int& bh, int& rb) 
 }
 
 // Load the B-operand chunks of one stationary 16-row block: lane l holds row
-// row0 + (l & 15), chunk kk at dims chunk_elem(kk, l >> 4).  Rows >= N read 0.
+// `row`, chunk kk = dims [kk*kKC + g*kKC/4, +kKC/4) with g = l >> 4.
+// Rows >= N read 0.
 template <typename T, int D, int NC>
 __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, int row, int N) {
   static_assert(NC == Geo<T, D>::kChunks, "chunk count");
@@ -189,49 +221,40 @@ __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, i
 #pragma unroll
   for (int kk = 0; kk < NC; ++kk) {
     if (row < N)
-      f[kk] = *(const u32x4*)(head + (int64_t)row * D + Geo<T, D>::chunk_elem(kk, g));
+      f[kk] = *(const u32x4*)(head + (int64_t)row * D + kk * Elt<T>::kKC + g * (Elt<T>::kKC / 4));
     else
       f[kk] = u32x4{0u, 0u, 0u, 0u};
   }
 }
 
-// Register-staged copy of NTENS streamed tiles (kBS rows x D each) from HBM to
-// LDS.  Rows >= N are zero-filled.  NT = threads in the workgroup.
-template <typename T, int D, int NT, int NTENS>
-struct TileCopy {
-  static constexpr int kCPR = Geo<T, D>::kCPR;
-  static constexpr int kNCH = kBS * kCPR;                       // chunks per tensor tile
-  static constexpr int kPer = (kNCH + NT - 1) / NT;
-  u32x4 r[NTENS][kPer];
+// Issue the HBM -> LDS copy of NTENS streamed tiles (rows s0 .. s0+kBS-1)
+// with global_load_lds_dwordx4: each wave instruction fills one contiguous
+// 1 KB block of the tile, lane i writing 16 bytes at offset 16*i, so the lane
+// fetches the logical chunk that belongs at that (swizzled) position.  Rows
+// >= N are clamped to row N-1 (finite data); every kernel masks them out.
+// The copy is asynchronous: call vm_wait() before the barrier that publishes it.
+template <typename T, int D, int NW, int NTENS>
+__device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N) {
+  using G = Geo<T, D>;
+  static_assert(G::kBlocks % NW == 0, "tile blocks per wave");
+  const int l = lane_id(), w = wave_id();
+#pragma unroll
+  for (int bi = 0; bi < G::kBlocks / NW; ++bi) {
+    const int b = w + bi * NW;
+    const int q = b * 64 + l;
+    const int r = q / G::kCPR;
+    const int c = (q % G::kCPR) ^ G::swz(r);
+    const int row = min(s0 + r, N - 1);
+#pragma unroll
+    for (int t = 0; t < NTENS; ++t)
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(src[t] + (int64_t)row * D + c * G::kEPC),
+          (__attribute__((address_space(3))) void*)(dst + t * G::kTileElems + b * (1024 / (int)sizeof(T))),
+          16, 0, 0);
+  }
+}
 
-  __device__ __forceinline__ void load(const T* const (&src)[NTENS], int s0, int N) {
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int c = threadIdx.x + i * NT;
-      const int row = c / kCPR, col = c - row * kCPR;
-      const bool ok = (c < kNCH) && (s0 + row < N);
-#pragma unroll
-      for (int t = 0; t < NTENS; ++t) {
-        if (ok)
-          r[t][i] = *(const u32x4*)(src[t] + (int64_t)(s0 + row) * D + col * (16 / (int)sizeof(T)));
-        else
-          r[t][i] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  }
-  __device__ __forceinline__ void store(T FB_LDS* dst) {
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int c = threadIdx.x + i * NT;
-      if (c < kNCH) {
-        const int row = c / kCPR, col = c - row * kCPR;
-#pragma unroll
-        for (int t = 0; t < NTENS; ++t)
-          *(u32x4 FB_LDS*)(dst + t * Geo<T, D>::kTileElems + row * Geo<T, D>::kLdx + col * (16 / (int)sizeof(T))) = r[t][i];
-      }
-    }
-  }
-};
+__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile: NS vectors of
 // kBS floats; entries >= N are zero.

@@ -15,13 +15,12 @@ namespace fb {
 // the log-normalizer of Sec. 2).  Stationary: query rows.  Streamed: K, V.
 // Online softmax with a running row max, as in FlashAttention.
 // ===========================================================================
-template <typename T, int D, int MR, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
+template <typename T, int D, int MR, int NW, int OCC>
+__global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
-  constexpr int NT = NW * 64;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
 
@@ -45,15 +44,14 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
   for (int mb = 0; mb < MR; ++mb) { mrun[mb] = -1e30f; lsum[mb] = 0.f; }
   const float c = scale * kLog2e;
 
-  TileCopy<T, D, NT, 2> cp;
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  cp.load(src, 0, N);
-  cp.store((T FB_LDS*)lds[0]);
+  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
+  vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
     const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* Vt = Kt + G::kTileElems;
 
@@ -66,7 +64,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int kk = 0; kk < G::kChunks; ++kk) {
-        const u32x4 a = *(const u32x4 FB_LDS*)(Kt + (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g));
+        const u32x4 a = *(const u32x4 FB_LDS*)(Kt + G::chunk_off(16 * sb + j, 4 * kk + g));
 #pragma unroll
         for (int mb = 0; mb < MR; ++mb) s[sb][mb] = E::mma_chunk(a, qf[mb][kk], s[sb][mb]);
       }
@@ -101,11 +99,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
     }
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag a = E::load_afrag(Vt, G::kLdx, 16 * nb);
+      const typename E::AFrag a = G::load_afrag(Vt, 16 * nb);
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, pf[mb], acc[nb][mb]);
     }
-    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    vm_wait();
     __syncthreads();
   }
 #pragma unroll
@@ -126,14 +124,13 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_fwd_kernel(
 // dS = P (dP - D), dP = dO V^T (eqs. 2-3).  Stationary: Q, dO rows.
 // Streamed: K, V.  Writes D and dQ once per row; no atomics.
 // ===========================================================================
-template <typename T, int D, int MR, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
+template <typename T, int D, int MR, int NW, int OCC>
+__global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const float* __restrict__ L,
     T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
-  constexpr int NT = NW * 64;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
 
@@ -167,15 +164,14 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
     for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
 
-  TileCopy<T, D, NT, 2> cp;
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  cp.load(src, 0, N);
-  cp.store((T FB_LDS*)lds[0]);
+  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
+  vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
     const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* Vt = Kt + G::kTileElems;
 
@@ -188,7 +184,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
         const u32x4 ak = *(const u32x4 FB_LDS*)(Kt + off);
         const u32x4 av = *(const u32x4 FB_LDS*)(Vt + off);
 #pragma unroll
@@ -210,11 +206,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
         }
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag a = E::load_afrag(Kt, G::kLdx, 16 * nb);
+      const typename E::AFrag a = G::load_afrag(Kt, 16 * nb);
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, dsf[mb], acc[nb][mb]);
     }
-    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    vm_wait();
     __syncthreads();
   }
 #pragma unroll
@@ -231,14 +227,13 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_rows_kernel(
 // First backward, column side: dV = P^T dO and dK = tau dS^T Q (eqs. 2-3).
 // Stationary: K, V rows.  Streamed: Q, dO tiles with their L and D.
 // ===========================================================================
-template <typename T, int D, int MC, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
+template <typename T, int D, int MC, int NW, int OCC>
+__global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
     T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
-  constexpr int NT = NW * 64;
   constexpr int BC = 16 * MC * NW;
   __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
   __shared__ __attribute__((aligned(16))) float sc[2][2 * kBS];
@@ -263,17 +258,16 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
     for (int mc = 0; mc < MC; ++mc) dk[nb][mc] = dv[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
 
-  TileCopy<T, D, NT, 2> cp;
   const T* const src[2] = {Q + hoff, dO + hoff};
   const float* const ssrc[2] = {L + soff, Dv + soff};
   const int nT = (N + kBS - 1) / kBS;
-  cp.load(src, 0, N);
-  cp.store((T FB_LDS*)lds[0]);
+  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
   copy_row_scalars<2>((float FB_LDS*)sc[0], ssrc, 0, N);
+  vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
     const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* dOs = Qs + G::kTileElems;
     const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
@@ -288,7 +282,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
         const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
         const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
 #pragma unroll
@@ -315,18 +309,16 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
     }
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag ado = E::load_afrag(dOs, G::kLdx, 16 * nb);
-      const typename E::AFrag aq = E::load_afrag(Qs, G::kLdx, 16 * nb);
+      const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
+      const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
 #pragma unroll
       for (int mc = 0; mc < MC; ++mc) {
         dv[nb][mc] = E::mma_acc(ado, pf[mc], dv[nb][mc]);
         dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
       }
     }
-    if (it + 1 < nT) {
-      cp.store((T FB_LDS*)lds[(it + 1) & 1]);
-      copy_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
-    }
+    if (it + 1 < nT) copy_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    vm_wait();
     __syncthreads();
   }
 #pragma unroll
@@ -346,23 +338,28 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bwd_cols_kernel(
 // BoB Pass 1 (row-major; Alg. 1/2 Pass 1 with the affine fusion of Prop. 3.1).
 // Stationary: Q, U_Q, dO rows (+ L, D).  Streamed: K, V, U_K, U_V.
 // Per tile it recomputes S, P, dP, F, C (as transposed tiles), forms
-// Pt0 = C + F (dP - D), and accumulates the six row accumulators
+// Pt0 = C + F (dP - D), and accumulates the row accumulators
 //   alpha += rowsum(P F),  E0 += rowsum(P Pt0),
 //   dOt0 += P U_V + (P F) V,  Omega += (P Pt0) K + (P (dP - D)) U_K,
 //   Bacc += P K,  R += (P dP) K.
 // Epilogue (eq. 8): E = E0 - alpha D, dOt = dOt0 - alpha O,
 // Qt = tau (Omega - alpha R - E Bacc).  Writes alpha, E, Qt, dOt once.
+//
+// kDQ variant: when the first-backward dQ is supplied, R is not accumulated.
+// Since dQ / tau = sum_j P (dP - D) k_j = R - D Bacc, eq. 8 becomes
+// Qt = tau (Omega - E0 Bacc) - alpha dQ with E0 = E + alpha D.  This drops one
+// B_r x d accumulator and one tile contraction per tile, which is what lets
+// the d = 128 kernel run two waves per SIMD.
 // ===========================================================================
-template <typename T, int D, int MR, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
+template <typename T, int D, int MR, int NW, int OCC, bool kDQ>
+__global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
     const T* __restrict__ UK, const T* __restrict__ UV, const float* __restrict__ L,
-    const float* __restrict__ Dv, T* __restrict__ Qt, T* __restrict__ dOt,
+    const float* __restrict__ Dv, const T* __restrict__ dQ, T* __restrict__ Qt, T* __restrict__ dOt,
     float* __restrict__ alpha_out, float* __restrict__ E_out, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
-  constexpr int NT = NW * 64;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[2][4 * G::kTileElems];
 
@@ -384,25 +381,29 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
     lb[mb] = row < N ? L[soff + row] * kLog2e : 0.f;
     drow[mb] = row < N ? Dv[soff + row] : 0.f;
   }
-  floatx4 aDO[G::kNB][MR], aOM[G::kNB][MR], aB[G::kNB][MR], aR[G::kNB][MR];
+  constexpr int kNR = kDQ ? 1 : G::kNB;  // R accumulator only in the six-accumulator form
+  floatx4 aDO[G::kNB][MR], aOM[G::kNB][MR], aB[G::kNB][MR], aR[kNR][MR];
 #pragma unroll
   for (int nb = 0; nb < G::kNB; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < MR; ++mb) aDO[nb][mb] = aOM[nb][mb] = aB[nb][mb] = aR[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int mb = 0; mb < MR; ++mb) aDO[nb][mb] = aOM[nb][mb] = aB[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int nb = 0; nb < kNR; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MR; ++mb) aR[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
   float alpha[MR], e0[MR];
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) alpha[mb] = e0[mb] = 0.f;
   const float c = scale * kLog2e;
 
-  TileCopy<T, D, NT, 4> cp;
   const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  cp.load(src, 0, N);
-  cp.store((T FB_LDS*)lds[0]);
+  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
+  vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
     const T FB_LDS* Ks = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* Vs = Ks + G::kTileElems;
     const T FB_LDS* UKs = Vs + G::kTileElems;
@@ -418,7 +419,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
         const u32x4 ak = *(const u32x4 FB_LDS*)(Ks + off);
         const u32x4 av = *(const u32x4 FB_LDS*)(Vs + off);
         const u32x4 auk = *(const u32x4 FB_LDS*)(UKs + off);
@@ -455,26 +456,26 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
           fPF[mb].set(i, pf);
           fPPt[mb].set(i, ppt);
           fPdd[mb].set(i, p * dd);
-          fPdp[mb].set(i, p * dpv);
+          if (!kDQ) fPdp[mb].set(i, p * dpv);
         }
     // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag ak = E::load_afrag(Ks, G::kLdx, 16 * nb);
-      const typename E::AFrag av = E::load_afrag(Vs, G::kLdx, 16 * nb);
-      const typename E::AFrag auk = E::load_afrag(UKs, G::kLdx, 16 * nb);
-      const typename E::AFrag auv = E::load_afrag(UVs, G::kLdx, 16 * nb);
+      const typename E::AFrag ak = G::load_afrag(Ks, 16 * nb);
+      const typename E::AFrag av = G::load_afrag(Vs, 16 * nb);
+      const typename E::AFrag auk = G::load_afrag(UKs, 16 * nb);
+      const typename E::AFrag auv = G::load_afrag(UVs, 16 * nb);
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) {
         aB[nb][mb] = E::mma_acc(ak, fP[mb], aB[nb][mb]);
-        aR[nb][mb] = E::mma_acc(ak, fPdp[mb], aR[nb][mb]);
+        if (!kDQ) aR[nb][mb] = E::mma_acc(ak, fPdp[mb], aR[nb][mb]);
         aOM[nb][mb] = E::mma_acc(ak, fPPt[mb], aOM[nb][mb]);
         aOM[nb][mb] = E::mma_acc(auk, fPdd[mb], aOM[nb][mb]);
         aDO[nb][mb] = E::mma_acc(auv, fP[mb], aDO[nb][mb]);
         aDO[nb][mb] = E::mma_acc(av, fPF[mb], aDO[nb][mb]);
       }
     }
-    if (it + 1 < nT) cp.store((T FB_LDS*)lds[(it + 1) & 1]);
+    vm_wait();
     __syncthreads();
   }
   // epilogue (eq. 8)
@@ -482,7 +483,8 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
   for (int mb = 0; mb < MR; ++mb) {
     const int row = row0 + 16 * mb + j;
     const float al = group_sum(alpha[mb]);
-    const float ee = group_sum(e0[mb]) - al * drow[mb];
+    const float e0s = group_sum(e0[mb]);
+    const float ee = e0s - al * drow[mb];
     if (row < N) {
       if (g == 0) {
         alpha_out[soff + row] = al;
@@ -493,7 +495,12 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
         const int64_t off = hoff + (int64_t)row * D + 16 * nb + 4 * g;
         const floatx4 o = E::load4(O + off);
         E::store4(dOt + off, aDO[nb][mb] - al * o);
-        E::store4(Qt + off, scale * (aOM[nb][mb] - al * aR[nb][mb] - ee * aB[nb][mb]));
+        if (kDQ) {
+          const floatx4 dq = E::load4(dQ + off);
+          E::store4(Qt + off, scale * (aOM[nb][mb] - e0s * aB[nb][mb]) - al * dq);
+        } else {
+          E::store4(Qt + off, scale * (aOM[nb][mb] - al * aR[kDQ ? 0 : nb][mb] - ee * aB[nb][mb]));
+        }
       }
     }
   }
@@ -506,8 +513,8 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass1_kernel(
 //   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
 // Writes Kt, Vt once; no atomics.
 // ===========================================================================
-template <typename T, int D, int MC, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
+template <typename T, int D, int MC, int NW, int OCC>
+__global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
@@ -515,7 +522,6 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
     T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
-  constexpr int NT = NW * 64;
   constexpr int BC = 16 * MC * NW;
   __shared__ __attribute__((aligned(16))) T lds[2][3 * G::kTileElems];
   __shared__ __attribute__((aligned(16))) float sc[2][4 * kBS];
@@ -543,17 +549,16 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
     for (int mc = 0; mc < MC; ++mc) aK[nb][mc] = aV[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
 
-  TileCopy<T, D, NT, 3> cp;
   const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
   const float* const ssrc[4] = {L + soff, Dv + soff, alpha_in + soff, E_in + soff};
   const int nT = (N + kBS - 1) / kBS;
-  cp.load(src, 0, N);
-  cp.store((T FB_LDS*)lds[0]);
+  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
   copy_row_scalars<4>((float FB_LDS*)sc[0], ssrc, 0, N);
+  vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) cp.load(src, s0 + kBS, N);
+    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
     const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* UQs = Qs + G::kTileElems;
     const T FB_LDS* dOs = UQs + G::kTileElems;
@@ -569,7 +574,7 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = (16 * sb + j) * G::kLdx + G::chunk_elem(kk, g);
+        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
         const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
         const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
         const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
@@ -608,9 +613,9 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
     }
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag aq = E::load_afrag(Qs, G::kLdx, 16 * nb);
-      const typename E::AFrag auq = E::load_afrag(UQs, G::kLdx, 16 * nb);
-      const typename E::AFrag ado = E::load_afrag(dOs, G::kLdx, 16 * nb);
+      const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
+      const typename E::AFrag auq = G::load_afrag(UQs, 16 * nb);
+      const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
 #pragma unroll
       for (int mc = 0; mc < MC; ++mc) {
         aV[nb][mc] = E::mma_acc(ado, fPh[mc], aV[nb][mc]);
@@ -618,10 +623,8 @@ __global__ __launch_bounds__(NW * 64, 1) void bob_pass2_kernel(
         aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
       }
     }
-    if (it + 1 < nT) {
-      cp.store((T FB_LDS*)lds[(it + 1) & 1]);
-      copy_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
-    }
+    if (it + 1 < nT) copy_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    vm_wait();
     __syncthreads();
   }
 #pragma unroll

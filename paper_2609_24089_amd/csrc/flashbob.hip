@@ -13,16 +13,16 @@ namespace {
 // wave, NW = waves per workgroup.  A workgroup owns 16*MR*NW stationary rows.
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 64> {
-  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 2, kP2MC = 2;
+  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 2, kP2MC = 2, kP1OccDQ = 1;
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 1, kP2MC = 1;
+  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 1, kP2MC = 1, kP1OccDQ = 2;
 };
 template <> struct Cfg<float, 64> {
-  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1;
+  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1, kP1OccDQ = 2;
 };
 template <> struct Cfg<float, 128> {
-  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1;
+  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1, kP1OccDQ = 1;
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -78,7 +78,7 @@ int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V
   using C = Cfg<T, D>;
   const Grid g = grid_for(p, 16 * C::kFwdMR * C::kNW);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((attn_fwd_kernel<T, D, C::kFwdMR, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((attn_fwd_kernel<T, D, C::kFwdMR, C::kNW, 1>), dim3(g.total), dim3(64 * C::kNW), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale);
   return finish_launch();
 }
@@ -90,13 +90,13 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
   using C = Cfg<T, D>;
   const Grid gr = grid_for(p, 16 * C::kRowsMR * C::kNW);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, C::kRowsMR, C::kNW>), dim3(gr.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, C::kRowsMR, C::kNW, 1>), dim3(gr.total), dim3(64 * C::kNW), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, L, (T*)dQ, Dv,
                      (int)p.N, gr.nRB, gr.total, p.scale);
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
   const Grid gc = grid_for(p, 16 * C::kColsMC * C::kNW);
-  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, C::kColsMC, C::kNW>), dim3(gc.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, C::kColsMC, C::kNW, 1>), dim3(gc.total), dim3(64 * C::kNW), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
                      (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale);
   return finish_launch();
@@ -105,14 +105,22 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
 template <typename T, int D>
 int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
                      const void* dO, const void* UQ, const void* UK, const void* UV, const float* L,
-                     const float* Dv, void* Qt, void* dOt, float* alpha, float* E, hipStream_t s) {
+                     const float* Dv, const void* dQ, void* Qt, void* dOt, float* alpha, float* E,
+                     hipStream_t s) {
   using C = Cfg<T, D>;
   const Grid g = grid_for(p, 16 * C::kP1MR * C::kNW);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, (const T*)UQ,
-                     (const T*)UK, (const T*)UV, L, Dv, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB,
-                     g.total, p.scale);
+  if (dQ != nullptr) {
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW, C::kP1OccDQ, true>), dim3(g.total),
+                       dim3(64 * C::kNW), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
+                       (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
+                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
+  } else {
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW, 1, false>), dim3(g.total),
+                       dim3(64 * C::kNW), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
+                       (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
+                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
+  }
   return finish_launch();
 }
 
@@ -123,7 +131,7 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
   using C = Cfg<T, D>;
   const Grid g = grid_for(p, 16 * C::kP2MC * C::kNW);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass2_kernel<T, D, C::kP2MC, C::kNW>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((bob_pass2_kernel<T, D, C::kP2MC, C::kNW, 2>), dim3(g.total), dim3(64 * C::kNW), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
                      (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale);
   return finish_launch();
@@ -172,15 +180,16 @@ int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, floa
 int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
                             const void* Q, const void* K, const void* V, const void* O,
                             const void* dO, const void* gdQ, const void* gdK, const void* gdV,
-                            const float* L, const float* D, void* Qt, void* dOt, float* alpha,
-                            float* E, void* stream) {
+                            const float* L, const float* D, const void* dQ, void* Qt, void* dOt,
+                            float* alpha, float* E, void* stream) {
   const Problem p{dtype, B, H, N, d, scale};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
   rc = fb::check_ptrs({Q, K, V, O, dO, gdQ, gdK, gdV, L, D, Qt, dOt, alpha, E});
   if (rc != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_pass1, p, Q, K, V, O, dO, gdQ, gdK, gdV, L, D, Qt, dOt, alpha, E,
+  if (dQ != nullptr && !fb::aligned16(dQ)) return BOB_EINVAL;
+  FB_DISPATCH(p, fb::launch_pass1, p, Q, K, V, O, dO, gdQ, gdK, gdV, L, D, dQ, Qt, dOt, alpha, E,
               (hipStream_t)stream);
 }
 

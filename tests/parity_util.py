@@ -37,8 +37,8 @@ def oracle_full(x, scale):
     return oracle.bob(*args, scale)
 
 
-def run_gpu_path(xd, scale):
+def run_gpu_path(xd, scale, use_dq=True):
     fb = lib()
-    out = fb.bob(*[xd[n] for n in NAMES], scale)
+    out = fb.bob(*[xd[n] for n in NAMES], scale, use_dq=use_dq)
     torch.cuda.synchronize()
     return out

@@ -54,7 +54,7 @@ MISALIGNED = (1 << 20) + 8
 
 
 def call(lib, fn, dtype=fb.BOB_BF16, B=1, H=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None):
-    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 14, "attn_bob_pass2_cols": 13}[fn]
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13}[fn]
     ptrs = [ctypes.c_void_p(ptr) for _ in range(nptr)]
     if bad_index is not None:
         ptrs[bad_index] = ctypes.c_void_p(0)
@@ -83,9 +83,19 @@ def test_rejects_bad_arguments_without_launching(lib, fn):
 
 @pytest.mark.parametrize("fn", FNS)
 def test_every_pointer_is_checked(lib, fn):
-    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 14, "attn_bob_pass2_cols": 13}[fn]
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13}[fn]
+    optional = {"attn_bob_pass1_rows": {10}}.get(fn, set())   # dQ may be NULL
     for i in range(nptr):
-        assert call(lib, fn, bad_index=i) == fb.BOB_EINVAL, i
+        if i not in optional:
+            assert call(lib, fn, bad_index=i) == fb.BOB_EINVAL, i
+
+
+def test_optional_dq_pointer(lib):
+    # NULL dQ selects the six-accumulator form; a misaligned dQ is rejected
+    assert call(lib, "attn_bob_pass1_rows", N=0, ptr=0) == fb.BOB_OK
+    ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(15)]
+    ptrs[10] = ctypes.c_void_p(MISALIGNED)
+    assert lib.attn_bob_pass1_rows(fb.BOB_BF16, 1, 1, 16, 64, ctypes.c_float(0.125), *ptrs, None) == fb.BOB_EINVAL
 
 
 @pytest.mark.parametrize("fn", FNS)

@@ -47,6 +47,22 @@ def test_full_path_matches_oracle(case):
         assert e <= TOL[dt], (k, e)
 
 
+@pytest.mark.parametrize("case", [(1, 1, 255, 64, "f32", 51), (1, 2, 300, 128, "f32", 52),
+                                  (2, 1, 257, 64, "bf16", 53), (1, 2, 513, 128, "bf16", 54)], ids=case_id)
+def test_six_accumulator_form_matches_oracle(case):
+    """Pass 1 without dQ: the six row accumulators of Prop. 3.1 (R accumulated)."""
+    B, H, N, d, dt, seed = case
+    say(f"[parity] six-accumulator Pass 1 {case_id(case)}")
+    x = make_inputs(B, H, N, d, dt, seed)
+    scale = 1.0 / np.sqrt(d)
+    ref = oracle_full(x, scale)
+    out = run_gpu_path(to_dev(x), scale, use_dq=False)
+    errs = {k: nrel(as_f64(out[k]), ref[k]) for k in ("Qt", "dOt", "alpha", "E", "Kt", "Vt")}
+    say("   errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL[dt], (k, e)
+
+
 @pytest.mark.parametrize("case", [(1, 1, 40, 64, "f32", 21), (1, 1, 200, 128, "bf16", 22),
                                   (2, 2, 130, 64, "bf16", 23)], ids=case_id)
 def test_bob_passes_with_oracle_row_state(case):
