@@ -141,15 +141,20 @@ template <> struct Elt<float> {
 
 // ---------------------------------------------------------------------------
 // LDS tile geometry.  A streamed tile is kBS rows x D elements, stored
-// without padding; the 16-byte chunks of row r are permuted by XOR with
-// swz(r) so that both access patterns are free of bank conflicts:
-//   * score A-operand reads (ds_read_b128): 16 lanes read one chunk from each
-//     of 16 consecutive rows -> swz must be a bijection on those rows;
-//   * transposed reads (ds_read_b64_tr_b16, bf16 only): 32 lanes read a
-//     32-byte chunk pair from each of 8 consecutive rows -> the pair index
-//     (c ^ swz(r)) >> 1 must differ across those rows.
-// fp32 tiles use swz(r) = r mod 16 (their accumulate operands are scalar
-// reads of one 64-byte run per row, which that also spreads).
+// without padding; the 16-byte chunks of each row are permuted (slot =
+// phys(r, c) for logical chunk c of row r) so that both LDS read patterns run
+// without bank conflicts.  What gfx950 needs, as measured with the
+// SQ_LDS_BANK_CONFLICT counter on probe patterns:
+//   * ds_read_b128 (score A-operands; lane (g, j) reads row j, chunk 4kk+g):
+//     within each group of 4 consecutive lanes the four 16-byte slots (mod
+//     256 bytes) must form two aligned 32-byte pairs;
+//   * ds_read_b64_tr_b16 (transposed accumulate operands; lane (g, j) reads 8
+//     bytes of row 4g + j/4): the 32 lanes served together must hit 32
+//     distinct 8-byte slots mod 256 bytes.
+// A per-row XOR cannot satisfy both, so bf16 rows use the permutations below
+// (row pairs share a 64-byte quad and differ in the low slot bit; successive
+// row pairs rotate through the quads).  fp32 tiles are only read with
+// ds_read_b128 and scalar loads and use slot = c ^ (r mod 16).
 // ---------------------------------------------------------------------------
 template <typename T, int D> struct Geo {
   static constexpr int kCPR = D * (int)sizeof(T) / 16;          // 16-byte chunks per row
@@ -159,18 +164,31 @@ template <typename T, int D> struct Geo {
   static constexpr int kNB = D / 16;                             // 16-dim output blocks
   static constexpr int kBlocks = kBS * kCPR / 64;                // 1 KB blocks per tile
 
-  static __device__ __forceinline__ int swz(int r) {
+  // physical slot of logical chunk c in row r
+  static __device__ __forceinline__ int phys(int r, int c) {
     if constexpr (sizeof(T) == 4) {
-      return r & 15;
+      return c ^ (r & 15);
     } else if constexpr (D == 128) {
-      return ((r & 7) << 1) | ((r >> 3) & 1);
+      return 4 * ((((r >> 1) & 3) + (c >> 1)) & 3) + 2 * (c & 1) + (((c >> 3) & 1) ^ (r & 1));
     } else {
       static_assert(D == 64, "head dim");
-      return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+      return 4 * ((((r >> 2) & 1) + (c >> 1)) & 1) + 2 * (c & 1) + (((c >> 2) & 1) ^ ((r >> 1) & 1));
+    }
+  }
+  // inverse: logical chunk stored at physical slot p of row r
+  static __device__ __forceinline__ int logical(int r, int p) {
+    if constexpr (sizeof(T) == 4) {
+      return p ^ (r & 15);
+    } else if constexpr (D == 128) {
+      const int nb = (((p & 1) ^ (r & 1)) << 2) | (((p >> 2) - ((r >> 1) & 3)) & 3);
+      return 2 * nb + ((p >> 1) & 1);
+    } else {
+      const int nb = (((p & 1) ^ ((r >> 1) & 1)) << 1) | ((p >> 2) ^ ((r >> 2) & 1));
+      return 2 * nb + ((p >> 1) & 1);
     }
   }
   // element offset of logical chunk c of tile row r
-  static __device__ __forceinline__ int chunk_off(int r, int c) { return r * D + ((c ^ swz(r)) * kEPC); }
+  static __device__ __forceinline__ int chunk_off(int r, int c) { return r * D + phys(r, c) * kEPC; }
 
   // score A-operand: row r, the lane group's chunk of MFMA step kk
   static __device__ __forceinline__ u32x4 read_chunk(const T FB_LDS* X, int r, int kk) {
@@ -230,7 +248,7 @@ __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, i
 // Issue the HBM -> LDS copy of NTENS streamed tiles (rows s0 .. s0+kBS-1)
 // with global_load_lds_dwordx4: each wave instruction fills one contiguous
 // 1 KB block of the tile, lane i writing 16 bytes at offset 16*i, so the lane
-// fetches the logical chunk that belongs at that (swizzled) position.  Rows
+// fetches the logical chunk that belongs at that (permuted) position.  Rows
 // >= N are clamped to row N-1 (finite data); every kernel masks them out.
 // The copy is asynchronous: call vm_wait() before the barrier that publishes it.
 template <typename T, int D, int NW, int NTENS>
@@ -243,7 +261,7 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
     const int b = w + bi * NW;
     const int q = b * 64 + l;
     const int r = q / G::kCPR;
-    const int c = (q % G::kCPR) ^ G::swz(r);
+    const int c = G::logical(r, q % G::kCPR);
     const int row = min(s0 + r, N - 1);
 #pragma unroll
     for (int t = 0; t < NTENS; ++t)
@@ -257,17 +275,22 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile: NS vectors of
-// kBS floats; entries >= N are zero.
+// kBS floats, copied HBM -> LDS with global_load_lds_dword (64 lanes x 4
+// bytes = two vectors per instruction, issued by waves 0 .. NS/2-1).  Indices
+// >= N are clamped to N-1; the kernels mask those rows.  Asynchronous like
+// issue_tiles().
 template <int NS>
-__device__ __forceinline__ void copy_row_scalars(float FB_LDS* dst, const float* const (&src)[NS], int s0, int N) {
-  const int t = threadIdx.x;
-  if (t < NS * kBS) {
-    const int v = t / kBS, i = t - v * kBS;
-    float x = 0.f;
+__device__ __forceinline__ void issue_row_scalars(float FB_LDS* dst, const float* const (&src)[NS], int s0, int N) {
+  static_assert(NS % 2 == 0 && kBS == 32, "two 32-float vectors per wave instruction");
+  const int w = wave_id(), l = lane_id();
 #pragma unroll
-    for (int u = 0; u < NS; ++u)
-      if (u == v && s0 + i < N) x = src[u][s0 + i];
-    dst[v * kBS + i] = x;
+  for (int k = 0; k < NS / 2; ++k) {
+    if (w == k) {
+      const int idx = min(s0 + (l & 31), N - 1);
+      const float* srcp = (l < 32) ? src[2 * k] : src[2 * k + 1];
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(srcp + idx),
+                                       (__attribute__((address_space(3))) void*)(dst + 64 * k), 4, 0, 0);
+    }
   }
 }
 

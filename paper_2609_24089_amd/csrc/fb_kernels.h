@@ -262,12 +262,15 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   const float* const ssrc[2] = {L + soff, Dv + soff};
   const int nT = (N + kBS - 1) / kBS;
   issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  copy_row_scalars<2>((float FB_LDS*)sc[0], ssrc, 0, N);
+  issue_row_scalars<2>((float FB_LDS*)sc[0], ssrc, 0, N);
   vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
+    if (it + 1 < nT) {
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
+      issue_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    }
     const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* dOs = Qs + G::kTileElems;
     const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
@@ -317,7 +320,6 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
         dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
       }
     }
-    if (it + 1 < nT) copy_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
     vm_wait();
     __syncthreads();
   }
@@ -553,12 +555,15 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const float* const ssrc[4] = {L + soff, Dv + soff, alpha_in + soff, E_in + soff};
   const int nT = (N + kBS - 1) / kBS;
   issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  copy_row_scalars<4>((float FB_LDS*)sc[0], ssrc, 0, N);
+  issue_row_scalars<4>((float FB_LDS*)sc[0], ssrc, 0, N);
   vm_wait();
   __syncthreads();
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
+    if (it + 1 < nT) {
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
+      issue_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    }
     const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
     const T FB_LDS* UQs = Qs + G::kTileElems;
     const T FB_LDS* dOs = UQs + G::kTileElems;
@@ -623,7 +628,6 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
         aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
       }
     }
-    if (it + 1 < nT) copy_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
     vm_wait();
     __syncthreads();
   }
