@@ -22,4 +22,6 @@ from .bob_oracle import (  # noqa: F401
     bob,
     bob_rows,
     bob_affine,
+    row_scalars,
+    bob_cols,
 )

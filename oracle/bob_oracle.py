@@ -289,3 +289,45 @@ def bob_rows(q, k, v, do, uq, uk, uv, tau, rows):
         dOt=P @ uv + (P * h) @ v,
         alpha=alpha, E=E, O=O, L=L, D=D, dQ=tau * (dS @ k),
     )
+
+
+def row_scalars(q, k, v, do, uq, uk, uv, tau, slab=1024):
+    """alpha, E, L, D for every query row of one head, computed slab by slab
+    with bob_rows (row-owned, so slabs are exact)."""
+    n = q.shape[0]
+    out = {key: np.empty(n) for key in ("alpha", "E", "L", "D")}
+    for r0 in range(0, n, slab):
+        rows = np.arange(r0, min(n, r0 + slab))
+        part = bob_rows(q, k, v, do, uq, uk, uv, tau, rows)
+        for key in out:
+            out[key][rows] = part[key]
+    return out
+
+
+def bob_cols(q, k, v, do, uq, uk, uv, tau, cols, alpha, E, L, D):
+    """Column-owned outputs of one head (Kt, Vt, and the producer's dK, dV) at
+    the key rows `cols`.
+
+    Column j sums over every query row i (Sec. 3.2: Kt and Vt "sum over rows
+    for each fixed column"), so the row scalars alpha, E, L, D of all rows are
+    inputs here; callers compute them with row_scalars() from this module.
+    The per-tile quantities follow the same definitions as bob_head, taken on
+    the N x |cols| slice of the attention matrices.
+    """
+    cols = np.asarray(cols)
+    kc, vc, ukc, uvc = k[cols], v[cols], uk[cols], uv[cols]
+    S = scores(q, kc, tau)
+    P = probabilities(S, L)
+    dP = dP_of(do, vc)
+    dS = dS_of(P, dP, D)
+    F = F_of(q, kc, uq, ukc, tau)
+    h = F - alpha[:, None]
+    C = C_of(do, uvc)
+    Pt = Ptilde_of(C, F, dP, D, alpha)
+    St = Stilde_of(P, Pt, E)
+    return dict(
+        Kt=tau * (St.T @ q + dS.T @ uq),
+        Vt=(P * h).T @ do,
+        dK=tau * (dS.T @ q),
+        dV=P.T @ do,
+    )

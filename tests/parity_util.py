@@ -42,3 +42,35 @@ def run_gpu_path(xd, scale, use_dq=True):
     out = fb.bob(*[xd[n] for n in NAMES], scale, use_dq=use_dq)
     torch.cuda.synchronize()
     return out
+
+
+def global_identities(x, out):
+    """I1, I2, I3 (scalar identities) and I5, I6 (zero column sums) evaluated
+    on device tensors in float64.  Returns {name: (lhs, rhs, scale)} for the
+    scalar identities, where `scale` is the size an inner product of
+    unrelated tensors of these norms would have (sum of norm products over
+    sqrt(numel)); and {name: max over heads of ||sum_j X_j|| / ||X||_F} for
+    the column sums.
+
+    The identities hold exactly for the BoB of attention: Phi is linear in dO
+    (I1); dQ, dK are linear in V and dV does not depend on V (I2); S is
+    unchanged by Q -> cQ, K -> K/c (I3); P and dS are unchanged by adding a
+    constant row to K or to V (I5, I6)."""
+    import math
+    ip = lambda a, b: float((a.double() * b.double()).sum())
+    nrm = lambda a: float(a.double().norm())
+    M = x["Q"].numel()
+    sq = math.sqrt(M)
+    dQUQ, dKUK, dVUV = ip(out["dQ"], x["UQ"]), ip(out["dK"], x["UK"]), ip(out["dV"], x["UV"])
+    sQ, sK, sV = nrm(out["dQ"]) * nrm(x["UQ"]), nrm(out["dK"]) * nrm(x["UK"]), nrm(out["dV"]) * nrm(x["UV"])
+    scal = {
+        "I1": (ip(x["dO"], out["dOt"]), dQUQ + dKUK + dVUV, (nrm(x["dO"]) * nrm(out["dOt"]) + sQ + sK + sV) / sq),
+        "I2": (ip(x["V"], out["Vt"]), dQUQ + dKUK, (nrm(x["V"]) * nrm(out["Vt"]) + sQ + sK) / sq),
+        "I3": (ip(x["Q"], out["Qt"]) - ip(x["K"], out["Kt"]), dKUK - dQUQ,
+               (nrm(x["Q"]) * nrm(out["Qt"]) + nrm(x["K"]) * nrm(out["Kt"]) + sQ + sK) / sq),
+    }
+    colsum = {}
+    for name in ("Kt", "Vt"):
+        t = out[name].double().flatten(0, 1)                 # [B*H, N, d]
+        colsum[name] = float((t.sum(1).norm(dim=-1) / t.norm(dim=(1, 2))).max())
+    return scal, colsum

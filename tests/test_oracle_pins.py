@@ -355,3 +355,20 @@ def test_golden_tiny_case_unchanged():
     out = bo.bob_head(*args, doc["tau"])
     for key, val in doc["outputs"].items():
         np.testing.assert_allclose(out[key], np.array(val), rtol=1e-13, atol=1e-14)
+
+
+def test_column_slices_match_full():
+    """bob_cols with row scalars from row_scalars (slabbed bob_rows) gives the
+    same Kt, Vt, dK, dV columns as the full materialised bob_head."""
+    rng = np.random.default_rng(16)
+    n, d = 90, 8
+    args = rand_inputs(n, d, rng)
+    tau = 1 / np.sqrt(d)
+    full = bo.bob_head(*args, tau)
+    rs = bo.row_scalars(*args, tau, slab=32)
+    for key in ("alpha", "E", "L", "D"):
+        assert rel(rs[key], full[key]) < 1e-13, key
+    cols = np.array([0, 5, 31, 32, 89])
+    part = bo.bob_cols(*args, tau, cols, rs["alpha"], rs["E"], rs["L"], rs["D"])
+    for key in ("Kt", "Vt", "dK", "dV"):
+        assert rel(part[key], full[key][cols]) < 1e-13, key
