@@ -250,7 +250,7 @@ __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, i
 // 1 KB block of the tile, lane i writing 16 bytes at offset 16*i, so the lane
 // fetches the logical chunk that belongs at that (permuted) position.  Rows
 // >= N are clamped to row N-1 (finite data); every kernel masks them out.
-// The copy is asynchronous: call vm_wait() before the barrier that publishes it.
+// The copy is asynchronous: wait_vm<>() before the barrier that publishes it.
 template <typename T, int D, int NW, int NTENS>
 __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N) {
   using G = Geo<T, D>;
@@ -272,7 +272,10 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
   }
 }
 
-__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (loads complete in issue order for this count).
+template <int N>
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile: NS vectors of
 // kBS floats, copied HBM -> LDS with global_load_lds_dword (64 lanes x 4

@@ -15,14 +15,14 @@ namespace fb {
 // the log-normalizer of Sec. 2).  Stationary: query rows.  Streamed: K, V.
 // Online softmax with a running row max, as in FlashAttention.
 // ===========================================================================
-template <typename T, int D, int MR, int NW, int OCC>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
-  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -46,13 +46,20 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  vm_wait();
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+  wait_vm<0>();
   __syncthreads();
+  int cur = 0;  // stage holding tile it
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
-    const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
+    const T FB_LDS* Kt = (const T FB_LDS*)lds[cur];
     const T FB_LDS* Vt = Kt + G::kTileElems;
 
     floatx4 s[2][MR];
@@ -103,8 +110,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, pf[mb], acc[nb][mb]);
     }
-    vm_wait();
+    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
+    if (NSTAGE == 3 && nx < nT)
+      wait_vm<kLT>();
+    else
+      wait_vm<0>();
     __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
@@ -124,7 +136,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 // dS = P (dP - D), dP = dO V^T (eqs. 2-3).  Stationary: Q, dO rows.
 // Streamed: K, V.  Writes D and dQ once per row; no atomics.
 // ===========================================================================
-template <typename T, int D, int MR, int NW, int OCC>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const float* __restrict__ L,
@@ -132,7 +144,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
-  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -166,13 +178,20 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  vm_wait();
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+  wait_vm<0>();
   __syncthreads();
+  int cur = 0;  // stage holding tile it
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
-    const T FB_LDS* Kt = (const T FB_LDS*)lds[it & 1];
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
+    const T FB_LDS* Kt = (const T FB_LDS*)lds[cur];
     const T FB_LDS* Vt = Kt + G::kTileElems;
 
     floatx4 s[2][MR], dp[2][MR];
@@ -210,8 +229,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, dsf[mb], acc[nb][mb]);
     }
-    vm_wait();
+    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
+    if (NSTAGE == 3 && nx < nT)
+      wait_vm<kLT>();
+    else
+      wait_vm<0>();
     __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
@@ -227,7 +251,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // First backward, column side: dV = P^T dO and dK = tau dS^T Q (eqs. 2-3).
 // Stationary: K, V rows.  Streamed: Q, dO tiles with their L and D.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
@@ -235,8 +259,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
-  __shared__ __attribute__((aligned(16))) T lds[2][2 * G::kTileElems];
-  __shared__ __attribute__((aligned(16))) float sc[2][2 * kBS];
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) float sc[NSTAGE][2 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -261,19 +285,28 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   const T* const src[2] = {Q + hoff, dO + hoff};
   const float* const ssrc[2] = {L + soff, Dv + soff};
   const int nT = (N + kBS - 1) / kBS;
-  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  issue_row_scalars<2>((float FB_LDS*)sc[0], ssrc, 0, N);
-  vm_wait();
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) {
+      issue_row_scalars<2>((float FB_LDS*)sc[st], ssrc, st * kBS, N);
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+    }
+  wait_vm<0>();
   __syncthreads();
+  int cur = 0;  // stage holding tile it
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) {
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
-      issue_row_scalars<2>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) {
+      issue_row_scalars<2>((float FB_LDS*)sc[nxs], ssrc, nx * kBS, N);
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
     }
-    const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
     const T FB_LDS* dOs = Qs + G::kTileElems;
-    const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
+    const float FB_LDS* Ls = (const float FB_LDS*)sc[cur];
     const float FB_LDS* Ds = Ls + kBS;
 
     floatx4 s[2][MC], dp[2][MC];
@@ -320,8 +353,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
         dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
       }
     }
-    vm_wait();
+    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
+    if (NSTAGE == 3 && nx < nT)
+      wait_vm<kLT>();
+    else
+      wait_vm<0>();
     __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
@@ -353,7 +391,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
 // B_r x d accumulator and one tile contraction per tile, which is what lets
 // the d = 128 kernel run two waves per SIMD.
 // ===========================================================================
-template <typename T, int D, int MR, int NW, int OCC, bool kDQ>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, bool kDQ>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
@@ -363,7 +401,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
-  __shared__ __attribute__((aligned(16))) T lds[2][4 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][4 * G::kTileElems];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -400,13 +438,20 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 
   const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  vm_wait();
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  constexpr int kLT = 4 * (G::kBlocks / NW);  // tile loads per wave per tile
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+  wait_vm<0>();
   __syncthreads();
+  int cur = 0;  // stage holding tile it
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
-    const T FB_LDS* Ks = (const T FB_LDS*)lds[it & 1];
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
+    const T FB_LDS* Ks = (const T FB_LDS*)lds[cur];
     const T FB_LDS* Vs = Ks + G::kTileElems;
     const T FB_LDS* UKs = Vs + G::kTileElems;
     const T FB_LDS* UVs = UKs + G::kTileElems;
@@ -477,8 +522,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         aDO[nb][mb] = E::mma_acc(av, fPF[mb], aDO[nb][mb]);
       }
     }
-    vm_wait();
+    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
+    if (NSTAGE == 3 && nx < nT)
+      wait_vm<kLT>();
+    else
+      wait_vm<0>();
     __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
   // epilogue (eq. 8)
 #pragma unroll
@@ -515,7 +565,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 //   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
 // Writes Kt, Vt once; no atomics.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
@@ -525,8 +575,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
-  __shared__ __attribute__((aligned(16))) T lds[2][3 * G::kTileElems];
-  __shared__ __attribute__((aligned(16))) float sc[2][4 * kBS];
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][3 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) float sc[NSTAGE][4 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -554,20 +604,29 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
   const float* const ssrc[4] = {L + soff, Dv + soff, alpha_in + soff, E_in + soff};
   const int nT = (N + kBS - 1) / kBS;
-  issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[0], 0, N);
-  issue_row_scalars<4>((float FB_LDS*)sc[0], ssrc, 0, N);
-  vm_wait();
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  constexpr int kLT = 3 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) {
+      issue_row_scalars<4>((float FB_LDS*)sc[st], ssrc, st * kBS, N);
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+    }
+  wait_vm<0>();
   __syncthreads();
+  int cur = 0;  // stage holding tile it
   for (int it = 0; it < nT; ++it) {
     const int s0 = it * kBS;
-    if (it + 1 < nT) {
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[(it + 1) & 1], s0 + kBS, N);
-      issue_row_scalars<4>((float FB_LDS*)sc[(it + 1) & 1], ssrc, s0 + kBS, N);
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) {
+      issue_row_scalars<4>((float FB_LDS*)sc[nxs], ssrc, nx * kBS, N);
+      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
     }
-    const T FB_LDS* Qs = (const T FB_LDS*)lds[it & 1];
+    const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
     const T FB_LDS* UQs = Qs + G::kTileElems;
     const T FB_LDS* dOs = UQs + G::kTileElems;
-    const float FB_LDS* Ls = (const float FB_LDS*)sc[it & 1];
+    const float FB_LDS* Ls = (const float FB_LDS*)sc[cur];
 
     // score tiles [s = query][t = key]
     floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
@@ -628,8 +687,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
         aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
       }
     }
-    vm_wait();
+    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
+    if (NSTAGE == 3 && nx < nT)
+      wait_vm<kLT>();
+    else
+      wait_vm<0>();
     __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {

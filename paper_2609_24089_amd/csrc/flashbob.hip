@@ -9,20 +9,29 @@
 namespace fb {
 namespace {
 
-// Launch shapes per (element type, head dim): MR/MC = 16-row MFMA blocks per
-// wave, NW = waves per workgroup.  A workgroup owns 16*MR*NW stationary rows.
+// Launch shapes per (element type, head dim) and kernel: MR = 16-row MFMA
+// blocks per wave, NW = waves per workgroup (a workgroup owns 16*MR*NW
+// stationary rows), OCC = waves per SIMD the register budget is held to, ST =
+// LDS pipeline stages (tiles in flight + 1).
+struct Shape {
+  int mr, nw, occ, st;
+};
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 64> {
-  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 2, kP2MC = 2, kP1OccDQ = 1;
+  static constexpr Shape kFwd{2, 4, 1, 2}, kRows{2, 4, 1, 2}, kCols{2, 4, 1, 2};
+  static constexpr Shape kP1{2, 4, 1, 2}, kP1Six{2, 4, 1, 2}, kP2{2, 4, 2, 3};
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr int kNW = 4, kFwdMR = 2, kRowsMR = 2, kColsMC = 2, kP1MR = 1, kP2MC = 1, kP1OccDQ = 2;
+  static constexpr Shape kFwd{2, 4, 1, 2}, kRows{2, 4, 1, 2}, kCols{2, 4, 1, 2};
+  static constexpr Shape kP1{1, 8, 2, 3}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 3};
 };
 template <> struct Cfg<float, 64> {
-  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1, kP1OccDQ = 2;
+  static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
 };
 template <> struct Cfg<float, 128> {
-  static constexpr int kNW = 4, kFwdMR = 1, kRowsMR = 1, kColsMC = 1, kP1MR = 1, kP2MC = 1, kP1OccDQ = 1;
+  static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -75,10 +84,10 @@ Grid grid_for(const Problem& p, int rows_per_block) {
 template <typename T, int D>
 int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V, void* O, float* L,
                    hipStream_t s) {
-  using C = Cfg<T, D>;
-  const Grid g = grid_for(p, 16 * C::kFwdMR * C::kNW);
+  constexpr Shape c = Cfg<T, D>::kFwd;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((attn_fwd_kernel<T, D, C::kFwdMR, C::kNW, 1>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((attn_fwd_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale);
   return finish_launch();
 }
@@ -87,16 +96,16 @@ template <typename T, int D>
 int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
                    const void* dO, const float* L, void* dQ, void* dK, void* dV, float* Dv,
                    hipStream_t s) {
-  using C = Cfg<T, D>;
-  const Grid gr = grid_for(p, 16 * C::kRowsMR * C::kNW);
+  constexpr Shape cr = Cfg<T, D>::kRows, cc = Cfg<T, D>::kCols;
+  const Grid gr = grid_for(p, 16 * cr.mr * cr.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, C::kRowsMR, C::kNW, 1>), dim3(gr.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, cr.mr, cr.nw, cr.occ, cr.st>), dim3(gr.total), dim3(64 * cr.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, L, (T*)dQ, Dv,
                      (int)p.N, gr.nRB, gr.total, p.scale);
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
-  const Grid gc = grid_for(p, 16 * C::kColsMC * C::kNW);
-  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, C::kColsMC, C::kNW, 1>), dim3(gc.total), dim3(64 * C::kNW), 0, s,
+  const Grid gc = grid_for(p, 16 * cc.mr * cc.nw);
+  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
                      (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale);
   return finish_launch();
@@ -107,17 +116,19 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
                      const void* dO, const void* UQ, const void* UK, const void* UV, const float* L,
                      const float* Dv, const void* dQ, void* Qt, void* dOt, float* alpha, float* E,
                      hipStream_t s) {
-  using C = Cfg<T, D>;
-  const Grid g = grid_for(p, 16 * C::kP1MR * C::kNW);
   (void)hipGetLastError();
   if (dQ != nullptr) {
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW, C::kP1OccDQ, true>), dim3(g.total),
-                       dim3(64 * C::kNW), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
+    constexpr Shape c = Cfg<T, D>::kP1;
+    const Grid g = grid_for(p, 16 * c.mr * c.nw);
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, true>), dim3(g.total),
+                       dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
                        (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
   } else {
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, C::kP1MR, C::kNW, 1, false>), dim3(g.total),
-                       dim3(64 * C::kNW), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
+    constexpr Shape c = Cfg<T, D>::kP1Six;
+    const Grid g = grid_for(p, 16 * c.mr * c.nw);
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, false>), dim3(g.total),
+                       dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
                        (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
   }
@@ -128,10 +139,10 @@ template <typename T, int D>
 int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
                      const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
                      const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s) {
-  using C = Cfg<T, D>;
-  const Grid g = grid_for(p, 16 * C::kP2MC * C::kNW);
+  constexpr Shape c = Cfg<T, D>::kP2;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass2_kernel<T, D, C::kP2MC, C::kNW, 2>), dim3(g.total), dim3(64 * C::kNW), 0, s,
+  hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
                      (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale);
   return finish_launch();
