@@ -277,24 +277,20 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
 template <int N>
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
-// Streamed per-row fp32 scalars (L, D, alpha, E) for one tile: NS vectors of
-// kBS floats, copied HBM -> LDS with global_load_lds_dword (64 lanes x 4
-// bytes = two vectors per instruction, issued by waves 0 .. NS/2-1).  Indices
-// >= N are clamped to N-1; the kernels mask those rows.  Asynchronous like
-// issue_tiles().
-template <int NS>
-__device__ __forceinline__ void issue_row_scalars(float FB_LDS* dst, const float* const (&src)[NS], int s0, int N) {
-  static_assert(NS % 2 == 0 && kBS == 32, "two 32-float vectors per wave instruction");
-  const int w = wave_id(), l = lane_id();
-#pragma unroll
-  for (int k = 0; k < NS / 2; ++k) {
-    if (w == k) {
-      const int idx = min(s0 + (l & 31), N - 1);
-      const float* srcp = (l < 32) ? src[2 * k] : src[2 * k + 1];
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(srcp + idx),
-                                       (__attribute__((address_space(3))) void*)(dst + 64 * k), 4, 0, 0);
-    }
-  }
+// Streamed per-row fp32 scalars (L, D, alpha, E) for one tile, copied HBM ->
+// LDS with global_load_lds_dword: one wave instruction moves two kBS-float
+// vectors (lanes 0..31 read `a`, lanes 32..63 read `b`) to dst[0 .. 63].
+// Indices >= N are clamped to N-1; the kernels mask those rows.  The two base
+// pointers are passed by value so that the per-lane choice is a register
+// select (an indexed pointer array would go through scratch memory and force
+// a full vmcnt wait).  Asynchronous like issue_tiles().
+__device__ __forceinline__ void issue_scalar_pair(float FB_LDS* dst, const float* a, const float* b, int s0, int N) {
+  static_assert(kBS == 32, "two 32-float vectors per wave instruction");
+  const int l = lane_id();
+  const int idx = min(s0 + (l & 31), N - 1);
+  const float* p = (l < 32 ? a : b) + idx;
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)p,
+                                   (__attribute__((address_space(3))) void*)dst, 4, 0, 0);
 }
 
 }  // namespace fb

@@ -283,14 +283,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   const float c = scale * kLog2e;
 
   const T* const src[2] = {Q + hoff, dO + hoff};
-  const float* const ssrc[2] = {L + soff, Dv + soff};
   const int nT = (N + kBS - 1) / kBS;
   static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
   constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
 #pragma unroll
   for (int st = 0; st < NSTAGE - 1; ++st)
     if (st < nT) {
-      issue_row_scalars<2>((float FB_LDS*)sc[st], ssrc, st * kBS, N);
+      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, st * kBS, N);
       issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
     }
   wait_vm<0>();
@@ -301,7 +300,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
     const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
     const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
     if (nx < nT) {
-      issue_row_scalars<2>((float FB_LDS*)sc[nxs], ssrc, nx * kBS, N);
+      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[nxs], L + soff, Dv + soff, nx * kBS, N);
       issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
     }
     const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
@@ -401,6 +400,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][4 * G::kTileElems];
 
   int bh, rb;
@@ -436,28 +436,15 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   for (int mb = 0; mb < MR; ++mb) alpha[mb] = e0[mb] = 0.f;
   const float c = scale * kLog2e;
 
-  const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
-  const int nT = (N + kBS - 1) / kBS;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
-  constexpr int kLT = 4 * (G::kBlocks / NW);  // tile loads per wave per tile
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int s0 = it * kBS;
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    const T FB_LDS* Ks = (const T FB_LDS*)lds[cur];
+  // transposed score tiles [s][t] = streamed . stationary, and the B-operand
+  // fragments the accumulate step consumes
+  floatx4 s[2][MR], dp[2][MR], f[2][MR], cc[2][MR];
+  typename E::TFrag fP[MR], fPF[MR], fPPt[MR], fPdd[MR], fPdp[MR];
+
+  auto score = [&](const T FB_LDS* Ks) {
     const T FB_LDS* Vs = Ks + G::kTileElems;
     const T FB_LDS* UKs = Vs + G::kTileElems;
     const T FB_LDS* UVs = UKs + G::kTileElems;
-
-    // transposed score tiles: [s][t] = streamed . stationary
-    floatx4 s[2][MR], dp[2][MR], f[2][MR], cc[2][MR];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -480,8 +467,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           cc[sb][mb] = E::mma_chunk(auv, dof[mb][kk], cc[sb][mb]);    // C^T = U_V dO^T
         }
       }
-    // elementwise: B-operand fragments for the accumulate step
-    typename E::TFrag fP[MR], fPF[MR], fPPt[MR], fPdd[MR], fPdp[MR];
+  };
+  auto elementwise = [&](int s0) {
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb)
 #pragma unroll
@@ -505,7 +492,12 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           fPdd[mb].set(i, p * dd);
           if (!kDQ) fPdp[mb].set(i, p * dpv);
         }
-    // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
+  };
+  // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
+  auto accumulate = [&](const T FB_LDS* Ks) {
+    const T FB_LDS* Vs = Ks + G::kTileElems;
+    const T FB_LDS* UKs = Vs + G::kTileElems;
+    const T FB_LDS* UVs = UKs + G::kTileElems;
 #pragma unroll
     for (int nb = 0; nb < G::kNB; ++nb) {
       const typename E::AFrag ak = G::load_afrag(Ks, 16 * nb);
@@ -522,6 +514,25 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         aDO[nb][mb] = E::mma_acc(av, fPF[mb], aDO[nb][mb]);
       }
     }
+  };
+
+  const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  constexpr int kLT = 4 * (G::kBlocks / NW);  // tile loads per wave per tile
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
+  wait_vm<0>();
+  __syncthreads();
+  int cur = 0;  // stage holding tile it
+  for (int it = 0; it < nT; ++it) {
+    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
+    const T FB_LDS* Ks = (const T FB_LDS*)lds[cur];
+    score(Ks);
+    elementwise(it * kBS);
+    accumulate(Ks);
     // tile it+1 must have landed; with three stages tile it+2 may still be in flight
     if (NSTAGE == 3 && nx < nT)
       wait_vm<kLT>();
@@ -602,14 +613,14 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const float c = scale * kLog2e;
 
   const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
-  const float* const ssrc[4] = {L + soff, Dv + soff, alpha_in + soff, E_in + soff};
   const int nT = (N + kBS - 1) / kBS;
   static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
   constexpr int kLT = 3 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
 #pragma unroll
   for (int st = 0; st < NSTAGE - 1; ++st)
     if (st < nT) {
-      issue_row_scalars<4>((float FB_LDS*)sc[st], ssrc, st * kBS, N);
+      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, st * kBS, N);
+      if (wave_id() == 1) issue_scalar_pair((float FB_LDS*)sc[st] + 2 * kBS, alpha_in + soff, E_in + soff, st * kBS, N);
       issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
     }
   wait_vm<0>();
@@ -620,7 +631,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
     const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
     if (nx < nT) {
-      issue_row_scalars<4>((float FB_LDS*)sc[nxs], ssrc, nx * kBS, N);
+      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[nxs], L + soff, Dv + soff, nx * kBS, N);
+      if (wave_id() == 1) issue_scalar_pair((float FB_LDS*)sc[nxs] + 2 * kBS, alpha_in + soff, E_in + soff, nx * kBS, N);
       issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
     }
     const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
