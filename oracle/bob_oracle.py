@@ -23,9 +23,21 @@ import numpy as np
 # --------------------------------------------------------------------------
 
 
-def scores(q, k, tau):
-    """S = tau * Q K^T (eq. 1, no mask: non-causal dense attention)."""
-    return tau * (q @ k.T)
+def scores(q, k, tau, causal=False, q_idx=None, k_idx=None):
+    """S = tau * Q K^T + M_mask (eq. 1).
+
+    Without a mask every key is valid.  With causal=True, M_mask is -inf
+    where the key index exceeds the query index (the causal pattern named in
+    Sec. 2), so P is zero there and every row sum runs over the valid set
+    V_i = {j <= i}.  q_idx / k_idx give the absolute indices of the rows of
+    q and k when they are slices (default: 0..n-1).
+    """
+    S = tau * (q @ k.T)
+    if causal:
+        qi = np.arange(q.shape[0]) if q_idx is None else np.asarray(q_idx)
+        kj = np.arange(k.shape[0]) if k_idx is None else np.asarray(k_idx)
+        S = np.where(kj[None, :] <= qi[:, None], S, -np.inf)
+    return S
 
 
 def log_normalizer(S):
@@ -39,12 +51,12 @@ def probabilities(S, L):
     return np.exp(S - L[:, None])
 
 
-def forward_head(q, k, v, tau):
-    """Eq. 1: S = tau Q K^T, P = softmax(S), O = P V; plus L.
+def forward_head(q, k, v, tau, causal=False):
+    """Eq. 1: S = tau Q K^T (+ mask), P = softmax(S), O = P V; plus L.
 
     Returns (O, L, P, S).
     """
-    S = scores(q, k, tau)
+    S = scores(q, k, tau, causal)
     L = log_normalizer(S)
     P = probabilities(S, L)
     O = P @ v
@@ -71,12 +83,12 @@ def dS_of(P, dP, D):
     return P * (dP - D[:, None])
 
 
-def first_backward_head(q, k, v, do, tau):
+def first_backward_head(q, k, v, do, tau, causal=False):
     """Eqs. 2-3 on one head, materialised.
 
     Returns a dict with O, L, P, S, dP, D, dS, dQ, dK, dV.
     """
-    O, L, P, S = forward_head(q, k, v, tau)
+    O, L, P, S = forward_head(q, k, v, tau, causal)
     dP = dP_of(do, v)
     D = row_D(P, dP)
     dS = dS_of(P, dP, D)
@@ -124,13 +136,14 @@ def Stilde_of(P, Pt, E):
     return P * (Pt - E[:, None])
 
 
-def bob_head(q, k, v, do, uq, uk, uv, tau):
+def bob_head(q, k, v, do, uq, uk, uv, tau, causal=False):
     """All four BoB outputs on one head, eqs. 6-7, fully materialised.
 
-    Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
-    O, L, D, dQ, dK, dV.
+    With causal=True the masked entries have P = 0, so every sum runs over
+    the valid columns of its row (Sec. 2 and App. A).  Returns a dict with
+    Qt, Kt, Vt, dOt, alpha, E and the producer state O, L, D, dQ, dK, dV.
     """
-    fb = first_backward_head(q, k, v, do, tau)
+    fb = first_backward_head(q, k, v, do, tau, causal)
     P, dP, D, dS = fb["P"], fb["dP"], fb["D"], fb["dS"]
     F = F_of(q, k, uq, uk, tau)
     alpha = alpha_of(P, F)
@@ -150,7 +163,7 @@ def bob_head(q, k, v, do, uq, uk, uv, tau):
     )
 
 
-def bob_affine_head(q, k, v, do, uq, uk, uv, tau):
+def bob_affine_head(q, k, v, do, uq, uk, uv, tau, causal=False):
     """Row-owned outputs through the affine fusion of Prop. 3.1 (eq. 8).
 
     The six row accumulators are the sums named in the proof of Prop. 3.1
@@ -160,7 +173,7 @@ def bob_affine_head(q, k, v, do, uq, uk, uv, tau):
     E, dOt and Qt.  Here the sums run over the whole row at once (no tiling),
     so this is a second route to the same numbers, not the tiled schedule.
     """
-    O, L, P, _ = forward_head(q, k, v, tau)
+    O, L, P, _ = forward_head(q, k, v, tau, causal)
     dP = dP_of(do, v)
     D = row_D(P, dP)
     F = F_of(q, k, uq, uk, tau)
@@ -188,27 +201,28 @@ def bob_affine_head(q, k, v, do, uq, uk, uv, tau):
 # --------------------------------------------------------------------------
 
 
-def first_backward_rowloop(q, k, v, do, tau):
+def first_backward_rowloop(q, k, v, do, tau, causal=False):
     n, d = q.shape
     dq = np.zeros_like(q)
     dk = np.zeros_like(k)
     dv = np.zeros_like(v)
     for i in range(n):
-        s = np.array([tau * float(np.dot(q[i], k[j])) for j in range(n)])
+        m = i + 1 if causal else n              # row i sees keys 0..m-1
+        s = np.array([tau * float(np.dot(q[i], k[j])) for j in range(m)])
         e = np.exp(s - s.max())
         p = e / e.sum()
-        grad_p = v @ do[i]                      # d<o_i, do_i>/dp_j = v_j . do_i
+        grad_p = v[:m] @ do[i]                  # d<o_i, do_i>/dp_j = v_j . do_i
         jac = np.diag(p) - np.outer(p, p)       # dp/ds for one softmax row
         grad_s = jac.T @ grad_p
-        dq[i] = tau * (grad_s @ k)
-        dk += tau * np.outer(grad_s, q[i])
-        dv += np.outer(p, do[i])
+        dq[i] = tau * (grad_s @ k[:m])
+        dk[:m] += tau * np.outer(grad_s, q[i])
+        dv[:m] += np.outer(p, do[i])
     return dq, dk, dv
 
 
-def phi_rowloop(q, k, v, do, uq, uk, uv, tau):
+def phi_rowloop(q, k, v, do, uq, uk, uv, tau, causal=False):
     """Phi of eq. 4 evaluated through the independent first backward."""
-    dq, dk, dv = first_backward_rowloop(q, k, v, do, tau)
+    dq, dk, dv = first_backward_rowloop(q, k, v, do, tau, causal)
     return float((dq * uq).sum() + (dk * uk).sum() + (dv * uv).sum())
 
 
@@ -222,10 +236,10 @@ def _heads(x):
     return x.reshape((-1,) + x.shape[-2:])
 
 
-def _batched(fn, keys, shapes_from, *mats, tau):
+def _batched(fn, keys, shapes_from, *mats, tau, causal=False):
     lead = shapes_from.shape[:-2]
     flat = [_heads(np.asarray(m, dtype=np.float64)) for m in mats]
-    outs = [fn(*[m[h] for m in flat], tau) for h in range(flat[0].shape[0])]
+    outs = [fn(*[m[h] for m in flat], tau, causal) for h in range(flat[0].shape[0])]
     res = {}
     for key in keys:
         arr = np.stack([o[key] for o in outs])
@@ -233,33 +247,33 @@ def _batched(fn, keys, shapes_from, *mats, tau):
     return res
 
 
-def forward(Q, K, V, tau):
+def forward(Q, K, V, tau, causal=False):
     """Batched eq. 1: returns dict(O, L)."""
-    def f(q, k, v, t):
-        O, L, _, _ = forward_head(q, k, v, t)
+    def f(q, k, v, t, c):
+        O, L, _, _ = forward_head(q, k, v, t, c)
         return dict(O=O, L=L)
-    return _batched(f, ("O", "L"), Q, Q, K, V, tau=tau)
+    return _batched(f, ("O", "L"), Q, Q, K, V, tau=tau, causal=causal)
 
 
-def first_backward(Q, K, V, dO, tau):
+def first_backward(Q, K, V, dO, tau, causal=False):
     """Batched eqs. 1-3: returns dict(O, L, D, dQ, dK, dV)."""
     keys = ("O", "L", "D", "dQ", "dK", "dV")
-    return _batched(first_backward_head, keys, Q, Q, K, V, dO, tau=tau)
+    return _batched(first_backward_head, keys, Q, Q, K, V, dO, tau=tau, causal=causal)
 
 
-def bob(Q, K, V, dO, UQ, UK, UV, tau):
+def bob(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
     """Batched BoB (eqs. 6-7): dict(Qt, Kt, Vt, dOt, alpha, E, O, L, D, dQ, dK, dV)."""
     keys = ("Qt", "Kt", "Vt", "dOt", "alpha", "E", "O", "L", "D", "dQ", "dK", "dV")
-    return _batched(bob_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau)
+    return _batched(bob_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau, causal=causal)
 
 
-def bob_affine(Q, K, V, dO, UQ, UK, UV, tau):
+def bob_affine(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
     """Batched Prop. 3.1 route: dict(Qt, dOt, alpha, E, E0)."""
     keys = ("Qt", "dOt", "alpha", "E", "E0")
-    return _batched(bob_affine_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau)
+    return _batched(bob_affine_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau, causal=causal)
 
 
-def bob_rows(q, k, v, do, uq, uk, uv, tau, rows):
+def bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal=False):
     """Row-owned outputs of one head restricted to the query rows `rows`.
 
     Every row-owned quantity (Qt, dOt, alpha, E, O, L, D, dQ) of row i depends
@@ -270,7 +284,7 @@ def bob_rows(q, k, v, do, uq, uk, uv, tau, rows):
     """
     rows = np.asarray(rows)
     qi, doi, uqi = q[rows], do[rows], uq[rows]
-    S = scores(qi, k, tau)
+    S = scores(qi, k, tau, causal, q_idx=rows)
     L = log_normalizer(S)
     P = probabilities(S, L)
     O = P @ v
@@ -291,20 +305,20 @@ def bob_rows(q, k, v, do, uq, uk, uv, tau, rows):
     )
 
 
-def row_scalars(q, k, v, do, uq, uk, uv, tau, slab=1024):
+def row_scalars(q, k, v, do, uq, uk, uv, tau, slab=1024, causal=False):
     """alpha, E, L, D for every query row of one head, computed slab by slab
     with bob_rows (row-owned, so slabs are exact)."""
     n = q.shape[0]
     out = {key: np.empty(n) for key in ("alpha", "E", "L", "D")}
     for r0 in range(0, n, slab):
         rows = np.arange(r0, min(n, r0 + slab))
-        part = bob_rows(q, k, v, do, uq, uk, uv, tau, rows)
+        part = bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal)
         for key in out:
             out[key][rows] = part[key]
     return out
 
 
-def bob_cols(q, k, v, do, uq, uk, uv, tau, cols, alpha, E, L, D):
+def bob_cols(q, k, v, do, uq, uk, uv, tau, cols, alpha, E, L, D, causal=False):
     """Column-owned outputs of one head (Kt, Vt, and the producer's dK, dV) at
     the key rows `cols`.
 
@@ -316,7 +330,7 @@ def bob_cols(q, k, v, do, uq, uk, uv, tau, cols, alpha, E, L, D):
     """
     cols = np.asarray(cols)
     kc, vc, ukc, uvc = k[cols], v[cols], uk[cols], uv[cols]
-    S = scores(q, kc, tau)
+    S = scores(q, kc, tau, causal, k_idx=cols)
     P = probabilities(S, L)
     dP = dP_of(do, vc)
     dS = dS_of(P, dP, D)

@@ -21,7 +21,7 @@ MUTATIONS = {
     "Stilde drops E": ("Stilde_of", lambda P, Pt, E: P * Pt),
     "E column sum": ("E_of", lambda P, Pt: np.broadcast_to((P * Pt).sum(axis=0), P.shape[:1]).copy()),
     "dS D sign": ("dS_of", lambda P, dP, D: P * (dP + D[:, None])),
-    "scores missing tau": ("scores", lambda q, k, tau: q @ k.T),
+    "scores missing tau": ("scores", lambda q, k, tau, *a, **kw: q @ k.T),
     "dP transposed": ("dP_of", lambda do, v: v @ do.T),
     "row D from P only": ("row_D", lambda P, dP: dP.sum(axis=-1)),
 }
