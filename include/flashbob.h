@@ -23,8 +23,12 @@
  *          Supported head dimensions: d = 64 and d = 128 (both dtypes).
  *  scale   the softmax scale tau of eq. 1 (the paper uses 1/sqrt(d)); any
  *          finite value is accepted.  L is the natural-log normalizer
- *          L_i = log sum_j exp(S_ij) with S = tau Q K^T.  No mask: every key
- *          is visible to every query (dense, non-causal attention).
+ *          L_i = log sum_{j valid} exp(S_ij) with S = tau Q K^T.
+ *  causal  0: no mask, every key is visible to every query (dense
+ *          attention).  1: the causal mask of eq. 1 (M_ij = -inf for j > i),
+ *          so every row sum runs over keys j <= i; the kernels skip tiles
+ *          above the diagonal.  All four calls of one problem must use the
+ *          same value.
  *  pointers  device pointers owned by the caller, 16-byte aligned.  The
  *          library allocates no memory and keeps no state.  Outputs must not
  *          alias inputs.
@@ -35,7 +39,8 @@
  *          or with events by the caller.
  *
  * Errors: every argument check happens before any HIP call, so a rejected
- * call has no effect.  BOB_EINVAL: negative B/H/N, non-finite scale, a NULL
+ * call has no effect.  BOB_EINVAL: negative B/H/N, non-finite scale, causal
+ * not 0/1, a NULL
  * or misaligned pointer for a non-empty problem, or a problem too large for
  * the launch grid.  BOB_EUNSUPPORTED: a (dtype, d) pair that is not built.
  * BOB_ELAUNCH: the HIP launch itself reported an error.  B*H*N == 0 is a
@@ -63,7 +68,7 @@ typedef enum {
 /* Forward attention (eq. 1) with its log-normalizer (Sec. 2).
  * In:  Q, K, V  [B,H,N,d].
  * Out: O = softmax(scale Q K^T) V  [B,H,N,d];  L (fp32 [B,H,N]). */
-int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                      const void* Q, const void* K, const void* V,
                      void* O, float* L, void* stream);
 
@@ -72,7 +77,7 @@ int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, 
  * Out: dQ, dK, dV [B,H,N,d];  D fp32 [B,H,N], D_i = do_i . o_i.
  * D is written by the row kernel before the column kernel reads it (both
  * are enqueued on `stream` by this call). */
-int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                  const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* L, void* dQ, void* dK, void* dV, float* D, void* stream);
 
@@ -86,7 +91,7 @@ int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, floa
  * With dQ given it drops R = sum_j P_ij dP_ij k_j, using R = dQ/scale + D B
  * (so Qt = scale (Omega - E0 B) - alpha dQ, E0 = E + alpha D); the result is
  * the same up to rounding and the d = 128 kernel fits two waves per SIMD. */
-int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                             const void* Q, const void* K, const void* V, const void* O,
                             const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                             const float* L, const float* D, const void* dQ,
@@ -95,7 +100,7 @@ int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
 /* BoB Pass 2, column-major (Alg. 1 Pass 2).
  * In:  Q, K, V, dO, gdQ, gdK, gdV [B,H,N,d];  L, D, alpha, E fp32 [B,H,N].
  * Out: Kt, Vt [B,H,N,d].  Must run after Pass 1 has written alpha and E. */
-int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                             const void* Q, const void* K, const void* V, const void* dO,
                             const void* gdQ, const void* gdK, const void* gdV,
                             const float* L, const float* D, const float* alpha, const float* E,

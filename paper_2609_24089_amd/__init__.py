@@ -32,7 +32,7 @@ def load_library():
             "(there is no non-HIP fallback)")
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
-    common = [i32, i64, i64, i64, i64, f32]
+    common = [i32, i64, i64, i64, i64, f32, i32]
     lib.attn_fwd_lse.argtypes = common + [vp] * 5 + [vp]
     lib.attn_bwd.argtypes = common + [vp] * 10 + [vp]
     lib.attn_bob_pass1_rows.argtypes = common + [vp] * 15 + [vp]
@@ -100,7 +100,7 @@ def _rows_empty(shape, like):
     return torch.empty(tuple(shape[:3]), dtype=torch.float32, device=like.device)
 
 
-def attn_fwd_lse(Q, K, V, scale, out=None, stream=None):
+def attn_fwd_lse(Q, K, V, scale, causal=False, out=None, stream=None):
     """Forward attention (eq. 1): returns (O, L)."""
     B, H, N, d = _check_mats(Q, K, V)
     if out is None:
@@ -109,12 +109,12 @@ def attn_fwd_lse(Q, K, V, scale, out=None, stream=None):
     _check_mats(Q, O)
     _check_rows(Q.shape, L)
     lib = load_library()
-    _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale),
+    _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
           _p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
     return O, L
 
 
-def attn_bwd(Q, K, V, O, dO, L, scale, out=None, stream=None):
+def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
     """First backward (eqs. 2-3): returns (dQ, dK, dV, D)."""
     B, H, N, d = _check_mats(Q, K, V, O, dO)
     _check_rows(Q.shape, L)
@@ -124,12 +124,13 @@ def attn_bwd(Q, K, V, O, dO, L, scale, out=None, stream=None):
     _check_mats(Q, dQ, dK, dV)
     _check_rows(Q.shape, D)
     lib = load_library()
-    _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale),
+    _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
           _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
     return dQ, dK, dV, D
 
 
-def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, dQ=None, out=None, stream=None):
+def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal=False, dQ=None, out=None,
+                        stream=None):
     """BoB Pass 1 (row-major): returns (Qt, dOt, alpha, E).
 
     dQ (the first-backward output) is optional; when given, the kernel uses
@@ -144,13 +145,13 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, dQ=None, out
     _check_mats(Q, Qt, dOt)
     _check_rows(Q.shape, alpha, E)
     lib = load_library()
-    _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale),
+    _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
           _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
           None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
     return Qt, dOt, alpha, E
 
 
-def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, out=None, stream=None):
+def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal=False, out=None, stream=None):
     """BoB Pass 2 (column-major): returns (Kt, Vt)."""
     B, H, N, d = _check_mats(Q, K, V, dO, gdQ, gdK, gdV)
     _check_rows(Q.shape, L, D, alpha, E)
@@ -159,13 +160,13 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, out=N
     Kt, Vt = out
     _check_mats(Q, Kt, Vt)
     lib = load_library()
-    _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale),
+    _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
           _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
           _p(Kt), _p(Vt), _stream(stream))
     return Kt, Vt
 
 
-def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, use_dq=True, stream=None):
+def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, use_dq=True, stream=None):
     """Whole path: forward, first backward, Pass 1, Pass 2 on one stream.
 
     use_dq=True hands the first-backward dQ to Pass 1 (five-accumulator form);
@@ -174,9 +175,9 @@ def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, use_dq=True, stream=None):
     Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
     O, L, D, dQ, dK, dV.
     """
-    O, L = attn_fwd_lse(Q, K, V, scale, stream=stream)
-    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, stream=stream)
-    Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale,
+    O, L = attn_fwd_lse(Q, K, V, scale, causal, stream=stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream)
+    Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal,
                                             dQ=dQ if use_dq else None, stream=stream)
-    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, stream=stream)
+    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)

@@ -222,12 +222,33 @@ template <typename T, int D> struct Geo {
 // Map a workgroup to (head, row block).  Workgroups are dispatched round-robin
 // over the 8 XCDs; when the count allows it, consecutive logical blocks (which
 // stream the same head's tensors) are kept on one XCD so they share its L2.
-__device__ __forceinline__ void map_block(int nRB, int total, int& bh, int& rb) {
+// With `reverse`, block indices run from the last block down (under a causal
+// mask the last query blocks carry the most tiles, so they start first).
+__device__ __forceinline__ void map_block(int nRB, int total, int& bh, int& rb, bool reverse = false) {
   int wg = blockIdx.x;
   int logical = ((total & 7) == 0) ? (wg & 7) * (total >> 3) + (wg >> 3) : wg;
   bh = logical / nRB;
   rb = logical - bh * nRB;
+  if (reverse) rb = nRB - 1 - rb;
 }
+
+// How a streamed tile of kBS rows starting at s0 meets one wave's stationary
+// rows [lo, hi] (N valid rows; causal mask: key <= query):
+//   0 = no valid element (skip the tile's math), 1 = every element valid,
+//   2 = mixed (mask per element).
+// Row-major kernels: stationary = query rows, streamed = key rows.
+__device__ __forceinline__ int tile_mode_rowmajor(int s0, int lo, int hi, int N, bool causal) {
+  if (causal && s0 > hi) return 0;
+  if (s0 + kBS <= N && (!causal || s0 + kBS - 1 <= lo)) return 1;
+  return 2;
+}
+// Column-major kernels: stationary = key rows, streamed = query rows.
+__device__ __forceinline__ int tile_mode_colmajor(int s0, int lo, int hi, int N, bool causal) {
+  if (causal && s0 + kBS - 1 < lo) return 0;
+  if (s0 + kBS <= N && (!causal || s0 >= hi)) return 1;
+  return 2;
+}
+
 
 // Load the B-operand chunks of one stationary 16-row block: lane l holds row
 // `row`, chunk kk = dims [kk*kKC + g*kKC/4, +kKC/4) with g = l >> 4.
@@ -277,6 +298,60 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
 template <int N>
 __device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 
+
+// Set the exponents of invalid (masked) tile entries to -inf, so exp2 gives
+// P = 0 there.  x[sb][m][r] belongs to streamed row s0 + 16 sb + 4 (l >> 4) + r
+// and stationary row t0 + 16 m, with t0 the lane's first stationary row.
+// Row-major kernels (stationary = query t, streamed = key s): valid iff
+// s < N and (no mask or s <= t).  Column-major kernels (stationary = key t,
+// streamed = query s): valid iff s < N and (no mask or s >= t).
+template <bool kRowMajor, int M>
+__device__ __forceinline__ void mask_tile(floatx4 (&x)[2][M], int s0, int t0, int N, bool causal) {
+  const int g = lane_id() >> 4;
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int sr = s0 + 16 * sb + 4 * g + r;
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const int t = t0 + 16 * m;
+        const bool ok = sr < N && (!causal || (kRowMajor ? sr <= t : sr >= t));
+        x[sb][m][r] = ok ? x[sb][m][r] : -INFINITY;
+      }
+    }
+}
+
+// The pipelined tile loop shared by every kernel: tiles it_begin .. it_end-1
+// stream through an NSTAGE-deep LDS ring.  issue(tile, stage) starts the
+// asynchronous copies of one tile (row scalars first, then the matrices, so
+// that at most LT loads per wave are younger than the previous tile's);
+// body(tile, stage) consumes a resident tile.  One barrier per tile.
+template <int NSTAGE, int LT, class Issue, class Body>
+__device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& issue, Body&& body) {
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  const int n = it_end - it_begin;
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < n) issue(it_begin + st, st);
+  wait_vm<0>();
+  __syncthreads();
+  int cur = 0;  // stage holding the current tile
+  for (int k = 0; k < n; ++k) {
+    const int nx = k + NSTAGE - 1;  // tile fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < n) issue(it_begin + nx, nxs);
+    body(it_begin + k, cur);
+    // the next tile must have landed; with three stages the one after it may
+    // still be in flight
+    if (NSTAGE == 3 && nx < n)
+      wait_vm<LT>();
+    else
+      wait_vm<0>();
+    __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
+  }
+}
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile, copied HBM ->
 // LDS with global_load_lds_dword: one wave instruction moves two kBS-float
 // vectors (lanes 0..31 read `a`, lanes 32..63 read `b`) to dst[0 .. 63].

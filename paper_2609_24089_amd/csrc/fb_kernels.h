@@ -5,27 +5,32 @@
 // (the paper's tilde-Q, tilde-K, tilde-V, tilde-dO).  All matrices are
 // [B*H, N, D] row-major; row scalars L, D, alpha, E are fp32 [B*H, N].
 // Softmax probabilities are recomputed from L as exp2(S*tau*log2e - L*log2e).
+//
+// Every kernel takes `causal`: without it every key is valid for every query;
+// with it the mask M_mask of eq. 1 is -inf where key > query, masked entries
+// get P = 0, tiles above the diagonal are skipped and diagonal tiles are
+// masked per element.  Rows past N are masked the same way.
 #pragma once
 #include "fb_common.h"
 
 namespace fb {
 
 // ===========================================================================
-// Forward: O = softmax(tau Q K^T) V and L = logsumexp(tau Q K^T)  (eq. 1 and
-// the log-normalizer of Sec. 2).  Stationary: query rows.  Streamed: K, V.
-// Online softmax with a running row max, as in FlashAttention.
+// Forward: O = softmax(tau Q K^T + M) V and L = logsumexp(tau Q K^T + M)
+// (eq. 1 and the log-normalizer of Sec. 2).  Stationary: query rows.
+// Streamed: K, V.  Online softmax with a running row max.
 // ===========================================================================
 template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
-    T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale) {
+    T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale, int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
 
   int bh, rb;
-  map_block(nRB, total, bh, rb);
+  map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int row0 = rb * BR + wave_id() * 16 * MR;
@@ -43,40 +48,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) { mrun[mb] = -1e30f; lsum[mb] = 0.f; }
   const float c = scale * kLog2e;
+  floatx4 s[2][MR];
+  typename E::TFrag pf[MR];
 
-  const T* const src[2] = {K + hoff, V + hoff};
-  const int nT = (N + kBS - 1) / kBS;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
-  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int s0 = it * kBS;
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    const T FB_LDS* Kt = (const T FB_LDS*)lds[cur];
-    const T FB_LDS* Vt = Kt + G::kTileElems;
-
-    floatx4 s[2][MR];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < G::kChunks; ++kk) {
-        const u32x4 a = *(const u32x4 FB_LDS*)(Kt + G::chunk_off(16 * sb + j, 4 * kk + g));
-#pragma unroll
-        for (int mb = 0; mb < MR; ++mb) s[sb][mb] = E::mma_chunk(a, qf[mb][kk], s[sb][mb]);
-      }
-
-    typename E::TFrag pf[MR];
+  // s holds log2-domain scores (masked entries -inf) when this runs
+  auto softmax_step = [&]() {
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb) {
       float x[8];
@@ -85,9 +61,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const bool ok = s0 + 16 * sb + 4 * g + r < N;
-          x[4 * sb + r] = ok ? s[sb][mb][r] * c : -INFINITY;
-          mx = fmaxf(mx, x[4 * sb + r]);
+          x[4 * sb + r] = s[sb][mb][r];
+          mx = fmaxf(mx, s[sb][mb][r]);
         }
       mx = group_max(mx);
       const float mnew = fmaxf(mrun[mb], mx);
@@ -104,20 +79,45 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 #pragma unroll
       for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
     }
+  };
+
+  const T* const src[2] = {K + hoff, V + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+      0, it_end,
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Ks = (const T FB_LDS*)lds[st];
+        const T FB_LDS* Vs = Ks + G::kTileElems;
 #pragma unroll
-    for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag a = G::load_afrag(Vt, 16 * nb);
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, pf[mb], acc[nb][mb]);
-    }
-    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
-    if (NSTAGE == 3 && nx < nT)
-      wait_vm<kLT>();
-    else
-      wait_vm<0>();
-    __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
-  }
+          for (int mb = 0; mb < MR; ++mb) s[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int kk = 0; kk < G::kChunks; ++kk) {
+            const u32x4 a = *(const u32x4 FB_LDS*)(Ks + G::chunk_off(16 * sb + j, 4 * kk + g));
+#pragma unroll
+            for (int mb = 0; mb < MR; ++mb) s[sb][mb] = E::mma_chunk(a, qf[mb][kk], s[sb][mb]);
+          }
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb) s[sb][mb] *= c;
+        if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
+        softmax_step();
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const typename E::AFrag a = G::load_afrag(Vs, 16 * nb);
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, pf[mb], acc[nb][mb]);
+        }
+      });
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
     const int row = row0 + 16 * mb + j;
@@ -140,14 +140,14 @@ template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const float* __restrict__ L,
-    T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale) {
+    T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale, int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
 
   int bh, rb;
-  map_block(nRB, total, bh, rb);
+  map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int row0 = rb * BR + wave_id() * 16 * MR;
@@ -175,68 +175,66 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
+  floatx4 s[2][MR], dp[2][MR];
+  typename E::TFrag dsf[MR];
 
-  const T* const src[2] = {K + hoff, V + hoff};
-  const int nT = (N + kBS - 1) / kBS;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
-  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int s0 = it * kBS;
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    const T FB_LDS* Kt = (const T FB_LDS*)lds[cur];
-    const T FB_LDS* Vt = Kt + G::kTileElems;
-
-    floatx4 s[2][MR], dp[2][MR];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-        const u32x4 ak = *(const u32x4 FB_LDS*)(Kt + off);
-        const u32x4 av = *(const u32x4 FB_LDS*)(Vt + off);
-#pragma unroll
-        for (int mb = 0; mb < MR; ++mb) {
-          s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);
-          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);
-        }
-      }
-    typename E::TFrag dsf[MR];
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
+  auto elementwise = [&]() {
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb)
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const bool ok = s0 + 16 * sb + 4 * g + r < N;
-          const float p = ok ? fast_exp2(s[sb][mb][r] * c - lb[mb]) : 0.f;
+          const float p = fast_exp2(s[sb][mb][r]);
           dsf[mb].set(4 * sb + r, p * (dp[sb][mb][r] - drow[mb]));
         }
+  };
+
+  const T* const src[2] = {K + hoff, V + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+      0, it_end,
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Ks = (const T FB_LDS*)lds[st];
+        const T FB_LDS* Vs = Ks + G::kTileElems;
 #pragma unroll
-    for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag a = G::load_afrag(Kt, 16 * nb);
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, dsf[mb], acc[nb][mb]);
-    }
-    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
-    if (NSTAGE == 3 && nx < nT)
-      wait_vm<kLT>();
-    else
-      wait_vm<0>();
-    __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
-  }
+          for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int kk = 0; kk < G::kChunks; ++kk) {
+            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+            const u32x4 ak = *(const u32x4 FB_LDS*)(Ks + off);
+            const u32x4 av = *(const u32x4 FB_LDS*)(Vs + off);
+#pragma unroll
+            for (int mb = 0; mb < MR; ++mb) {
+              s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);
+              dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);
+            }
+          }
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[sb][mb][r] = __builtin_fmaf(s[sb][mb][r], c, -lb[mb]);
+        if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
+        elementwise();
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const typename E::AFrag a = G::load_afrag(Ks, 16 * nb);
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb) acc[nb][mb] = E::mma_acc(a, dsf[mb], acc[nb][mb]);
+        }
+      });
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
     const int row = row0 + 16 * mb + j;
@@ -255,7 +253,7 @@ template <typename T, int D, int MC, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
-    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale) {
+    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
@@ -281,85 +279,80 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
 #pragma unroll
     for (int mc = 0; mc < MC; ++mc) dk[nb][mc] = dv[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
+  floatx4 s[2][MC], dp[2][MC];
+  typename E::TFrag pf[MC], dsf[MC];
 
-  const T* const src[2] = {Q + hoff, dO + hoff};
-  const int nT = (N + kBS - 1) / kBS;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
-  constexpr int kLT = 2 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) {
-      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, st * kBS, N);
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-    }
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int s0 = it * kBS;
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) {
-      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[nxs], L + soff, Dv + soff, nx * kBS, N);
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    }
-    const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
-    const T FB_LDS* dOs = Qs + G::kTileElems;
-    const float FB_LDS* Ls = (const float FB_LDS*)sc[cur];
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
+  auto elementwise = [&](const float FB_LDS* Ls) {
     const float FB_LDS* Ds = Ls + kBS;
-
-    floatx4 s[2][MC], dp[2][MC];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-        const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
-        const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
-#pragma unroll
-        for (int mc = 0; mc < MC; ++mc) {
-          s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);
-          dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
-        }
-      }
-    typename E::TFrag pf[MC], dsf[MC];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
-      const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
       const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ds + 16 * sb + 4 * g);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool ok = s0 + 16 * sb + 4 * g + r < N;
+      for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
-          const float p = ok ? fast_exp2(s[sb][mc][r] * c - lv[r] * kLog2e) : 0.f;
+          const float p = fast_exp2(s[sb][mc][r]);
           pf[mc].set(4 * sb + r, p);
           dsf[mc].set(4 * sb + r, p * (dp[sb][mc][r] - dv4[r]));
         }
-      }
     }
+  };
+
+  const T* const src[2] = {Q + hoff, dO + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_begin = causal ? (rb * BC) / kBS : 0;
+  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+      it_begin, nT,
+      [&](int it, int st) {
+        if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N);
+      },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
+        const T FB_LDS* dOs = Qs + G::kTileElems;
 #pragma unroll
-    for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
-      const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int mc = 0; mc < MC; ++mc) {
-        dv[nb][mc] = E::mma_acc(ado, pf[mc], dv[nb][mc]);
-        dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
-      }
-    }
-    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
-    if (NSTAGE == 3 && nx < nT)
-      wait_vm<kLT>();
-    else
-      wait_vm<0>();
-    __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
-  }
+          for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int kk = 0; kk < G::kChunks; ++kk) {
+            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+            const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+            const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc) {
+              s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);
+              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
+            }
+          }
+        const float FB_LDS* Ls = (const float FB_LDS*)sc[st];
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) {
+          const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+#pragma unroll
+          for (int mc = 0; mc < MC; ++mc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, -lv[r] * kLog2e);
+        }
+        if (mode == 2) mask_tile<false>(s, s0, col0 + j, N, causal != 0);
+        elementwise(Ls);
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
+          const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
+#pragma unroll
+          for (int mc = 0; mc < MC; ++mc) {
+            dv[nb][mc] = E::mma_acc(ado, pf[mc], dv[nb][mc]);
+            dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
+          }
+        }
+      });
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
     const int col = col0 + 16 * mc + j;
@@ -396,15 +389,15 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
     const T* __restrict__ UK, const T* __restrict__ UV, const float* __restrict__ L,
     const float* __restrict__ Dv, const T* __restrict__ dQ, T* __restrict__ Qt, T* __restrict__ dOt,
-    float* __restrict__ alpha_out, float* __restrict__ E_out, int N, int nRB, int total, float scale) {
+    float* __restrict__ alpha_out, float* __restrict__ E_out, int N, int nRB, int total, float scale,
+    int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][4 * G::kTileElems];
 
   int bh, rb;
-  map_block(nRB, total, bh, rb);
+  map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
   const int64_t soff = (int64_t)bh * N;
   const int l = lane_id(), g = l >> 4, j = l & 15;
@@ -468,15 +461,15 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         }
       }
   };
-  auto elementwise = [&](int s0) {
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
+  auto elementwise = [&]() {
 #pragma unroll
-    for (int mb = 0; mb < MR; ++mb)
+    for (int mb = 0; mb < MR; ++mb) {
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const bool ok = s0 + 16 * sb + 4 * g + r < N;
-          const float p = ok ? fast_exp2(s[sb][mb][r] * c - lb[mb]) : 0.f;
+          const float p = fast_exp2(s[sb][mb][r]);
           const float fv = f[sb][mb][r] * scale;
           const float dpv = dp[sb][mb][r];
           const float dd = dpv - drow[mb];
@@ -492,6 +485,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           fPdd[mb].set(i, p * dd);
           if (!kDQ) fPdp[mb].set(i, p * dpv);
         }
+    }
   };
   // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
   auto accumulate = [&](const T FB_LDS* Ks) {
@@ -518,29 +512,27 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 
   const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
   const int nT = (N + kBS - 1) / kBS;
-  constexpr int kLT = 4 * (G::kBlocks / NW);  // tile loads per wave per tile
+  const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  stream_loop<NSTAGE, 4 * (G::kBlocks / NW)>(
+      0, it_end,
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Ks = (const T FB_LDS*)lds[st];
+        score(Ks);
 #pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    const T FB_LDS* Ks = (const T FB_LDS*)lds[cur];
-    score(Ks);
-    elementwise(it * kBS);
-    accumulate(Ks);
-    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
-    if (NSTAGE == 3 && nx < nT)
-      wait_vm<kLT>();
-    else
-      wait_vm<0>();
-    __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
-  }
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[sb][mb][r] = __builtin_fmaf(s[sb][mb][r], c, -lb[mb]);
+        if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
+        elementwise();
+        accumulate(Ks);
+      });
+
   // epilogue (eq. 8)
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
@@ -582,7 +574,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
     const float* __restrict__ alpha_in, const float* __restrict__ E_in,
-    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale) {
+    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
@@ -611,71 +603,21 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
 #pragma unroll
     for (int mc = 0; mc < MC; ++mc) aK[nb][mc] = aV[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
   const float c = scale * kLog2e;
+  floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
+  typename E::TFrag fPh[MC], fSt[MC], fdS[MC];
 
-  const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
-  const int nT = (N + kBS - 1) / kBS;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
-  constexpr int kLT = 3 * (G::kBlocks / NW);  // tile loads per wave per tile (after its scalar load)
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < nT) {
-      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, st * kBS, N);
-      if (wave_id() == 1) issue_scalar_pair((float FB_LDS*)sc[st] + 2 * kBS, alpha_in + soff, E_in + soff, st * kBS, N);
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], st * kBS, N);
-    }
-  wait_vm<0>();
-  __syncthreads();
-  int cur = 0;  // stage holding tile it
-  for (int it = 0; it < nT; ++it) {
-    const int s0 = it * kBS;
-    const int nx = it + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < nT) {
-      if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[nxs], L + soff, Dv + soff, nx * kBS, N);
-      if (wave_id() == 1) issue_scalar_pair((float FB_LDS*)sc[nxs] + 2 * kBS, alpha_in + soff, E_in + soff, nx * kBS, N);
-      issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[nxs], nx * kBS, N);
-    }
-    const T FB_LDS* Qs = (const T FB_LDS*)lds[cur];
-    const T FB_LDS* UQs = Qs + G::kTileElems;
-    const T FB_LDS* dOs = UQs + G::kTileElems;
-    const float FB_LDS* Ls = (const float FB_LDS*)sc[cur];
-
-    // score tiles [s = query][t = key]
-    floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = f[sb][mc] = cc[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-        const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
-        const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
-        const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
-#pragma unroll
-        for (int mc = 0; mc < MC; ++mc) {
-          s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
-          dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP = dO V^T
-          f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // U_Q K^T
-          f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       // + Q U_K^T
-          cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C = dO U_V^T
-        }
-      }
-    typename E::TFrag fPh[MC], fSt[MC], fdS[MC];
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
+  auto elementwise = [&](const float FB_LDS* Ls) {
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
-      const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
       const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ls + kBS + 16 * sb + 4 * g);
       const floatx4 av4 = *(const floatx4 FB_LDS*)(Ls + 2 * kBS + 16 * sb + 4 * g);
       const floatx4 ev4 = *(const floatx4 FB_LDS*)(Ls + 3 * kBS + 16 * sb + 4 * g);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const bool ok = s0 + 16 * sb + 4 * g + r < N;
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
-          const float p = ok ? fast_exp2(s[sb][mc][r] * c - lv[r] * kLog2e) : 0.f;
+          const float p = fast_exp2(s[sb][mc][r]);
           const float fv = f[sb][mc][r] * scale;
           const float dpv = dp[sb][mc][r];
           const float dd = dpv - dv4[r];
@@ -687,26 +629,72 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
         }
       }
     }
+  };
+
+  const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_begin = causal ? (rb * BC) / kBS : 0;
+  stream_loop<NSTAGE, 3 * (G::kBlocks / NW)>(
+      it_begin, nT,
+      [&](int it, int st) {
+        if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);
+        if (wave_id() == 1)
+          issue_scalar_pair((float FB_LDS*)sc[st] + 2 * kBS, alpha_in + soff, E_in + soff, it * kBS, N);
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N);
+      },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
+        const T FB_LDS* UQs = Qs + G::kTileElems;
+        const T FB_LDS* dOs = UQs + G::kTileElems;
+        // score tiles [s = query][t = key]
 #pragma unroll
-    for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
-      const typename E::AFrag auq = G::load_afrag(UQs, 16 * nb);
-      const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
+        for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int mc = 0; mc < MC; ++mc) {
-        aV[nb][mc] = E::mma_acc(ado, fPh[mc], aV[nb][mc]);
-        aK[nb][mc] = E::mma_acc(aq, fSt[mc], aK[nb][mc]);
-        aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
-      }
-    }
-    // tile it+1 must have landed; with three stages tile it+2 may still be in flight
-    if (NSTAGE == 3 && nx < nT)
-      wait_vm<kLT>();
-    else
-      wait_vm<0>();
-    __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
-  }
+          for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = f[sb][mc] = cc[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int kk = 0; kk < G::kChunks; ++kk) {
+            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+            const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+            const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
+            const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+            for (int mc = 0; mc < MC; ++mc) {
+              s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
+              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP = dO V^T
+              f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // U_Q K^T
+              f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       // + Q U_K^T
+              cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C = dO U_V^T
+            }
+          }
+        const float FB_LDS* Ls = (const float FB_LDS*)sc[st];
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) {
+          const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+#pragma unroll
+          for (int mc = 0; mc < MC; ++mc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, -lv[r] * kLog2e);
+        }
+        if (mode == 2) mask_tile<false>(s, s0, col0 + j, N, causal != 0);
+        elementwise(Ls);
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
+          const typename E::AFrag auq = G::load_afrag(UQs, 16 * nb);
+          const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
+#pragma unroll
+          for (int mc = 0; mc < MC; ++mc) {
+            aV[nb][mc] = E::mma_acc(ado, fPh[mc], aV[nb][mc]);
+            aK[nb][mc] = E::mma_acc(aq, fSt[mc], aK[nb][mc]);
+            aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
+          }
+        }
+      });
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
     const int col = col0 + 16 * mc + j;

@@ -42,6 +42,7 @@ struct Problem {
   int32_t dtype;
   int64_t B, H, N, d;
   float scale;
+  int32_t causal;
 };
 
 // Returns BOB_OK to proceed, or an error; sets *empty for B*H*N == 0.
@@ -50,6 +51,7 @@ int32_t check_problem(const Problem& p, bool* empty) {
   if (p.dtype != BOB_F32 && p.dtype != BOB_BF16) return BOB_EINVAL;
   if (p.B < 0 || p.H < 0 || p.N < 0 || p.d < 1) return BOB_EINVAL;
   if (!std::isfinite(p.scale)) return BOB_EINVAL;
+  if (p.causal != 0 && p.causal != 1) return BOB_EINVAL;
   if (p.d != 64 && p.d != 128) return BOB_EUNSUPPORTED;
   if (p.B == 0 || p.H == 0 || p.N == 0) {
     *empty = true;
@@ -88,7 +90,7 @@ int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V
   const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_fwd_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale);
+                     (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale, p.causal);
   return finish_launch();
 }
 
@@ -101,13 +103,13 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, cr.mr, cr.nw, cr.occ, cr.st>), dim3(gr.total), dim3(64 * cr.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, L, (T*)dQ, Dv,
-                     (int)p.N, gr.nRB, gr.total, p.scale);
+                     (int)p.N, gr.nRB, gr.total, p.scale, p.causal);
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
   const Grid gc = grid_for(p, 16 * cc.mr * cc.nw);
   hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
-                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale);
+                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal);
   return finish_launch();
 }
 
@@ -123,14 +125,14 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
     hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, true>), dim3(g.total),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
-                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
+                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
     hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, false>), dim3(g.total),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
-                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale);
+                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
   }
   return finish_launch();
 }
@@ -144,7 +146,7 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
   (void)hipGetLastError();
   hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
-                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale);
+                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal);
   return finish_launch();
 }
 
@@ -165,9 +167,9 @@ using fb::Problem;
 
 extern "C" {
 
-int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                      const void* Q, const void* K, const void* V, void* O, float* L, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale};
+  const Problem p{dtype, B, H, N, d, scale, causal};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -176,10 +178,10 @@ int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, 
   FB_DISPATCH(p, fb::launch_fwd, p, Q, K, V, O, L, (hipStream_t)stream);
 }
 
-int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                  const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale};
+  const Problem p{dtype, B, H, N, d, scale, causal};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -188,12 +190,12 @@ int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, floa
   FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream);
 }
 
-int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                             const void* Q, const void* K, const void* V, const void* O,
                             const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                             const float* L, const float* D, const void* dQ, void* Qt, void* dOt,
                             float* alpha, float* E, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale};
+  const Problem p{dtype, B, H, N, d, scale, causal};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -204,12 +206,12 @@ int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
               (hipStream_t)stream);
 }
 
-int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                             const void* Q, const void* K, const void* V, const void* dO,
                             const void* gdQ, const void* gdK, const void* gdV, const float* L,
                             const float* D, const float* alpha, const float* E, void* Kt, void* Vt,
                             void* stream) {
-  const Problem p{dtype, B, H, N, d, scale};
+  const Problem p{dtype, B, H, N, d, scale, causal};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;

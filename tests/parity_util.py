@@ -32,14 +32,14 @@ def nrel(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
-def oracle_full(x, scale):
+def oracle_full(x, scale, causal=False):
     args = [as_f64(x[n]) for n in NAMES]
-    return oracle.bob(*args, scale)
+    return oracle.bob(*args, scale, causal=causal)
 
 
-def run_gpu_path(xd, scale, use_dq=True):
+def run_gpu_path(xd, scale, use_dq=True, causal=False):
     fb = lib()
-    out = fb.bob(*[xd[n] for n in NAMES], scale, use_dq=use_dq)
+    out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal, use_dq=use_dq)
     torch.cuda.synchronize()
     return out
 

@@ -53,12 +53,12 @@ ALIGNED = 1 << 20          # fake, 16-byte aligned addresses: never dereferenced
 MISALIGNED = (1 << 20) + 8
 
 
-def call(lib, fn, dtype=fb.BOB_BF16, B=1, H=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None):
+def call(lib, fn, dtype=fb.BOB_BF16, B=1, H=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None, causal=0):
     nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13}[fn]
     ptrs = [ctypes.c_void_p(ptr) for _ in range(nptr)]
     if bad_index is not None:
         ptrs[bad_index] = ctypes.c_void_p(0)
-    return getattr(lib, fn)(dtype, B, H, N, d, ctypes.c_float(scale), *ptrs, None)
+    return getattr(lib, fn)(dtype, B, H, N, d, ctypes.c_float(scale), causal, *ptrs, None)
 
 
 FNS = ["attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"]
@@ -79,6 +79,8 @@ def test_rejects_bad_arguments_without_launching(lib, fn):
     assert call(lib, fn, ptr=0) == fb.BOB_EINVAL
     assert call(lib, fn, N=(1 << 30) + 1) == fb.BOB_EINVAL
     assert call(lib, fn, B=1 << 20, H=1 << 20) == fb.BOB_EINVAL
+    assert call(lib, fn, causal=2) == fb.BOB_EINVAL
+    assert call(lib, fn, causal=-1) == fb.BOB_EINVAL
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -95,7 +97,7 @@ def test_optional_dq_pointer(lib):
     assert call(lib, "attn_bob_pass1_rows", N=0, ptr=0) == fb.BOB_OK
     ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(15)]
     ptrs[10] = ctypes.c_void_p(MISALIGNED)
-    assert lib.attn_bob_pass1_rows(fb.BOB_BF16, 1, 1, 16, 64, ctypes.c_float(0.125), *ptrs, None) == fb.BOB_EINVAL
+    assert lib.attn_bob_pass1_rows(fb.BOB_BF16, 1, 1, 16, 64, ctypes.c_float(0.125), 0, *ptrs, None) == fb.BOB_EINVAL
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -106,6 +108,7 @@ def test_empty_problem_is_a_no_op(lib, fn):
     assert call(lib, fn, H=0, d=128, ptr=0) == fb.BOB_OK
     # an unsupported head dim is reported even for an empty problem
     assert call(lib, fn, N=0, d=80, ptr=0) == fb.BOB_EUNSUPPORTED
+    assert call(lib, fn, N=0, ptr=0, causal=1) == fb.BOB_OK
 
 
 def test_binding_rejects_cpu_tensors():
