@@ -10,13 +10,16 @@ measured with HIP events around the two passes inside every timed step
 (median over steps).  `ms_per_step` is the wall time of the whole step.
 
 Prints ONE JSON line.  Default workload: B=1, H=16, N=16384, d=128, bf16
-(Q, K ~ 0.5*N(0,1), the rest N(0,1), seed 2).
+(Q, K ~ 0.5*N(0,1), the rest N(0,1), seed 2).  Under the causal mask the FLOP
+counts use the N(N+1)/2 unmasked (query, key) pairs per head instead of N^2.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --peak-n     # longest N (B=H=1, d=64) under a 60 s BoB cap
 """
 import argparse
 import hashlib
 import json
+import math
 import os
 import statistics
 import sys
@@ -38,6 +41,18 @@ NOMINAL_BOB_COEF = 38
 
 KERNEL_SOURCES = ["fb_common.h", "fb_kernels.h", "flashbob.hip"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+PEAK_N_FILE = os.path.join(ROOT, "profiles", "peak_n.json")
+
+# The paper's own attention-layer BoB times (Table 1: one A100 80GB, Triton,
+# causal, B=4, H=12, d=64, bf16 inputs), in ms, keyed by N.  Context only: other
+# hardware, and the paper does not say whether the time includes fwd/bwd.
+PAPER_TABLE1_MS = {256: 0.94, 512: 1.29, 1024: 2.57, 2048: 7.53, 4096: 25.80, 8192: 95.11,
+                   16384: 365.73, 32768: 1449.06, 65536: 5843.14, 131072: 23528.87, 262144: 94853.72}
+
+
+def pair_count(N, causal):
+    """(query, key) pairs that carry a nonzero P per head: N^2, or N(N+1)/2 causal."""
+    return N * (N + 1) / 2.0 if causal else float(N) * N
 
 
 def kernel_source_hash():
@@ -68,7 +83,7 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
     workload: the row-owned BoB outputs (Qt, dOt, alpha, E) of consecutive
     `slab`-row query slabs, head after head, until about `budget_s` seconds of
     CPU work are done.  Rate = Pass-1 executed FLOPs of those rows
-    (22 * rows * N * d) / time."""
+    (22 * d * the number of keys each row sees) / time."""
     import numpy as np
     from oracle import bob_rows
     from workloads import NAMES, as_f64
@@ -78,7 +93,7 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
     slab = min(slab, w.N)
-    rows, dt, heads_used = 0, 0.0, 0
+    rows, keys, dt, heads_used = 0, 0, 0.0, 0
     for b in range(w.B):
         for h in range(w.H):
             mats = [as_f64(x_cpu[n][b, h]) for n in NAMES]
@@ -86,16 +101,17 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
             for r0 in range(0, w.N, slab):
                 sel = np.arange(r0, min(w.N, r0 + slab))
                 t0 = time.perf_counter()
-                bob_rows(*mats, w.scale, sel)
+                bob_rows(*mats, w.scale, sel, causal=w.causal)
                 dt += time.perf_counter() - t0
                 rows += len(sel)
+                keys += int((sel + 1).sum()) if w.causal else len(sel) * w.N
                 if dt >= budget_s:
                     break
             if dt >= budget_s:
                 break
         if dt >= budget_s:
             break
-    flops = 22.0 * rows * w.N * w.d
+    flops = 22.0 * keys * w.d
     return {
         "value": round(flops / dt / 1e12, 6),
         "unit": "TFLOP/s",
@@ -103,8 +119,137 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
         "kind": "oracle",
         "sample": (f"float64 oracle bob_rows on {rows} query rows ({slab}-row slabs over {heads_used} "
                    f"head(s)) of {w.name}: row-owned outputs Qt, dOt, alpha, E in {dt:.1f} s; rate counts "
-                   f"the Pass-1 FLOPs 22*rows*N*d; BLAS threads={threads}, host cores={os.cpu_count()}"),
+                   f"the Pass-1 FLOPs 22*d*(keys seen by those rows); BLAS threads={threads}, host cores={os.cpu_count()}"),
     }
+
+
+def identity_checks(x, out):
+    """The BoB identities I1-I3 (scalar) and I5, I6 (zero column sums of Kt,
+    Vt), evaluated in float64 on device.  They hold exactly for any N, so they
+    check the full outputs at sizes no oracle reaches.  Returns the normalized
+    residuals: |lhs - rhs| / (the size of an inner product of unrelated tensors
+    of these norms), and max over heads of ||sum_j X_j|| / ||X||_F."""
+    ip = lambda a, b: float((a.double() * b.double()).sum())
+    nrm = lambda a: float(a.double().norm())
+    sq = math.sqrt(x["Q"].numel())
+    dQUQ, dKUK, dVUV = ip(out["dQ"], x["UQ"]), ip(out["dK"], x["UK"]), ip(out["dV"], x["UV"])
+    sQ, sK, sV = nrm(out["dQ"]) * nrm(x["UQ"]), nrm(out["dK"]) * nrm(x["UK"]), nrm(out["dV"]) * nrm(x["UV"])
+    res = {
+        "I1": abs(ip(x["dO"], out["dOt"]) - (dQUQ + dKUK + dVUV)) * sq / (nrm(x["dO"]) * nrm(out["dOt"]) + sQ + sK + sV),
+        "I2": abs(ip(x["V"], out["Vt"]) - (dQUQ + dKUK)) * sq / (nrm(x["V"]) * nrm(out["Vt"]) + sQ + sK),
+        "I3": abs(ip(x["Q"], out["Qt"]) - ip(x["K"], out["Kt"]) - (dKUK - dQUQ)) * sq
+        / (nrm(x["Q"]) * nrm(out["Qt"]) + nrm(x["K"]) * nrm(out["Kt"]) + sQ + sK),
+    }
+    for name, key in (("Kt", "I5"), ("Vt", "I6")):
+        t = out[name].double().flatten(0, 1)
+        res[key] = float((t.sum(1).norm(dim=-1) / t.norm(dim=(1, 2))).max())
+    return res
+
+
+IDENTITY_TOL = {"I1": 5e-3, "I2": 5e-3, "I3": 5e-3}
+# I5, I6 are reported, not gating, in the sweep: beyond N ~ 2^19 a one-sided
+# rounding bias of the MFMA fp32 accumulation (~1e-5 per element) adds up N
+# times in a column sum; the long-N GPU test checks columns against the oracle.
+
+
+class Path:
+    """Device buffers for one workload and one pass of the whole path."""
+
+    def __init__(self, fb, torch, x, w, dev):
+        self.fb, self.w, self.x = fb, w, x
+        Q = x["Q"]
+        rows_shape = (w.B, w.H, w.N)
+        E_ = lambda: torch.empty_like(Q)
+        R_ = lambda: torch.empty(rows_shape, dtype=torch.float32, device=dev)
+        self.O, self.L = E_(), R_()
+        self.dQ, self.dK, self.dV, self.D = E_(), E_(), E_(), R_()
+        self.Qt, self.dOt, self.alpha, self.E = E_(), E_(), R_(), R_()
+        self.Kt, self.Vt = E_(), E_()
+
+    def step(self, ev):
+        fb, x, s, c = self.fb, self.x, self.w.scale, self.w.causal
+        Q, K, V, dO, UQ, UK, UV = (x[n] for n in ("Q", "K", "V", "dO", "UQ", "UK", "UV"))
+        ev[0].record()
+        fb.attn_fwd_lse(Q, K, V, s, causal=c, out=(self.O, self.L))
+        ev[1].record()
+        fb.attn_bwd(Q, K, V, self.O, dO, self.L, s, causal=c, out=(self.dQ, self.dK, self.dV, self.D))
+        ev[2].record()
+        fb.attn_bob_pass1_rows(Q, K, V, self.O, dO, UQ, UK, UV, self.L, self.D, s, causal=c, dQ=self.dQ,
+                               out=(self.Qt, self.dOt, self.alpha, self.E))
+        ev[3].record()
+        fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, self.L, self.D, self.alpha, self.E, s, causal=c,
+                               out=(self.Kt, self.Vt))
+        ev[4].record()
+
+    def outputs(self):
+        return {"dQ": self.dQ, "dK": self.dK, "dV": self.dV, "Qt": self.Qt, "Kt": self.Kt,
+                "Vt": self.Vt, "dOt": self.dOt}
+
+
+def peak_n_sweep(args, log):
+    """Double N from 2^18 (B=H=1, d=64, bf16, dense) while the BoB time
+    (Pass 1 + Pass 2) stays within the cap and the buffers fit in HBM; every N
+    is checked with the identities I1-I3 on its full outputs (I5, I6 are
+    reported).  Stops before running an N whose predicted BoB time (4x the
+    previous) exceeds the cap."""
+    import torch
+    import paper_2609_24089_amd as fb
+    from workloads import Workload, workload_inputs
+    fb.load_library()
+    dev = torch.device("cuda:0")
+    free, total = torch.cuda.mem_get_info(dev)
+    results, N, best = [], args.peak_n_start, None
+    while True:
+        w = Workload(f"bf16_b1h1_n{N}_d64", 1, 1, N, 64, "bf16", 7)
+        need = 16 * N * 64 * 2 + 4 * 4 * N + 3 * N * 64 * 8   # buffers + float64 temporaries of the checks
+        if need > 0.9 * free:
+            log(f"N={N}: needs {need / 2**30:.1f} GiB of {free / 2**30:.1f} GiB free; stop")
+            break
+        log(f"N={N}: generating inputs")
+        x = {k: v.to(dev) for k, v in workload_inputs(w).items()}
+        path = Path(fb, torch, x, w, dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        torch.cuda.synchronize(dev)
+        log(f"N={N}: running the path")
+        path.step(ev)
+        torch.cuda.synchronize(dev)
+        per = [ev[i].elapsed_time(ev[i + 1]) / 1e3 for i in range(4)]
+        bob_s = per[2] + per[3]
+        res = identity_checks(x, path.outputs())
+        ok = all(res[k] <= IDENTITY_TOL[k] for k in IDENTITY_TOL)
+        tf = NOMINAL_BOB_COEF * float(N) ** 2 * 64 / bob_s / 1e12
+        ent = {"N": N, "bob_s": round(bob_s, 3), "step_s": round(sum(per), 3), "bob_tflops": round(tf, 1),
+               "identities": {k: float(f"{v:.2e}") for k, v in res.items()}, "identities_ok": ok,
+               "within_cap": bob_s <= args.peak_n_cap}
+        results.append(ent)
+        log(f"N={N}: BoB {bob_s:.2f} s ({tf:.0f} TF/s), identities {'ok' if ok else 'FAILED'} "
+            f"{ent['identities']}")
+        if ok and bob_s <= args.peak_n_cap:
+            best = N
+        del path, x
+        torch.cuda.empty_cache()
+        if not ok or bob_s > args.peak_n_cap or 4 * bob_s > args.peak_n_cap:
+            break
+        N *= 2
+    line = {"metric": f"peak N on one GPU: longest N (B=H=1, d=64, bf16, dense) whose BoB (Pass 1 + Pass 2) "
+                      f"finishes within {args.peak_n_cap:.0f} s and passes identities I1-I3",
+            "value": best, "unit": "tokens", "cap_s": args.peak_n_cap,
+            "hbm_bytes_per_token": 16 * 64 * 2 + 16,
+            "hbm_total_gib": round(total / 2**30, 1),
+            "memory_bound_n_estimate": int(0.9 * total / (16 * 64 * 2 + 16)),
+            "sweep": results, "source_hash": kernel_source_hash()}
+    print(json.dumps(line), flush=True)
+
+
+def peak_n_summary():
+    """The committed peak-N sweep, if it was taken on the current kernels."""
+    try:
+        doc = json.load(open(PEAK_N_FILE))
+    except (OSError, ValueError):
+        return None
+    return {"value": doc.get("value"), "unit": "tokens", "cap_s": doc.get("cap_s"),
+            "current": doc.get("source_hash") == kernel_source_hash(),
+            "source": "profiles/peak_n.json (bench.py --peak-n)"}
 
 
 def main():
@@ -117,32 +262,31 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (counter calibration)")
+    ap.add_argument("--peak-n", action="store_true", help="run the peak-N sweep instead of the step benchmark")
+    ap.add_argument("--peak-n-start", type=int, default=1 << 18)
+    ap.add_argument("--peak-n-cap", type=float, default=60.0)
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "gpus_requested": args.gpus}))
         sys.exit(2)
 
+    log = lambda msg: print(f"[bench] {msg}", file=sys.stderr, flush=True)
+    if args.peak_n:
+        peak_n_sweep(args, log)
+        return
+
     import torch
     import paper_2609_24089_amd as fb
     from workloads import WORKLOADS, workload_inputs
 
-    log = lambda msg: print(f"[bench] {msg}", file=sys.stderr, flush=True)
     fb.load_library()
     w = WORKLOADS[args.workload]
     log(f"workload {w.name}: generating inputs")
     x_cpu = workload_inputs(w)
     dev = torch.device("cuda:0")
     x = {k: v.to(dev) for k, v in x_cpu.items()}
-    Q, K, V, dO, UQ, UK, UV = (x[n] for n in ("Q", "K", "V", "dO", "UQ", "UK", "UV"))
-    rows_shape = (w.B, w.H, w.N)
-    E_ = lambda: torch.empty_like(Q)
-    R_ = lambda: torch.empty(rows_shape, dtype=torch.float32, device=dev)
-    O, L = E_(), R_()
-    dQ, dK, dV, Dv = E_(), E_(), E_(), R_()
-    Qt, dOt, alpha, Eb = E_(), E_(), R_(), R_()
-    Kt, Vt = E_(), E_()
-    s = w.scale
+    path = Path(fb, torch, x, w, dev)
 
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib * 2**20 // 4
@@ -153,27 +297,16 @@ def main():
         del src, dst
         log(f"copy calibration: {args.copy_calibration_mib} MiB read + written")
 
-    def step(ev):
-        ev[0].record()
-        fb.attn_fwd_lse(Q, K, V, s, out=(O, L))
-        ev[1].record()
-        fb.attn_bwd(Q, K, V, O, dO, L, s, out=(dQ, dK, dV, Dv))
-        ev[2].record()
-        fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, Dv, s, dQ=dQ, out=(Qt, dOt, alpha, Eb))
-        ev[3].record()
-        fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, Dv, alpha, Eb, s, out=(Kt, Vt))
-        ev[4].record()
-
     mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(5)]
     torch.cuda.reset_peak_memory_stats(dev)
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
-        step(mk())
+        path.step(mk())
     events = [mk() for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(events[k])
+        path.step(events[k])
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
     log(f"timed {args.steps} steps in {wall:.2f} s")
@@ -183,7 +316,7 @@ def main():
     bob_ms = sorted(a + b for a, b in zip(per["pass1"], per["pass2"]))
     q = lambda xs, f: xs[min(len(xs) - 1, int(f * len(xs)))]
     bob_med = statistics.median(bob_ms)
-    unit = w.B * w.H * float(w.N) ** 2 * w.d
+    unit = w.B * w.H * pair_count(w.N, w.causal) * w.d
     peak = PEAK_TFLOPS[w.dtype]
     value = NOMINAL_BOB_COEF * unit / (bob_med * 1e-3) / 1e12
     kern = {}
@@ -197,6 +330,7 @@ def main():
     achieved = FLOP_COEF[dom] * unit / (dom_ms * 1e-3) / 1e12
     traffic = measured_traffic(dom, w.name)
     step_flops = sum(FLOP_COEF.values()) * unit
+    nsq = "N(N+1)/2" if w.causal else "N^2"
 
     line = {
         "metric": "BoB TFLOP/s (38*B*H*N^2*d / time of Pass 1 + Pass 2) and % of MI355X dense bf16 MFMA peak",
@@ -212,20 +346,32 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "scale": w.scale,
-                   "seed": w.seed, "qk_scale": w.qk_scale, "causal": False},
+                   "seed": w.seed, "qk_scale": w.qk_scale, "causal": w.causal},
         "pct_peak": round(100.0 * value / peak, 2),
         "bob_ms": {"median": round(bob_med, 4), "p20": round(q(bob_ms, 0.2), 4),
                    "p80": round(q(bob_ms, 0.8), 4)},
         "bob_tflops_min_count": round(24.0 * unit / (bob_med * 1e-3) / 1e12, 2),
         "bob_tflops_executed": round((FLOP_COEF["pass1"] + FLOP_COEF["pass2"]) * unit / (bob_med * 1e-3) / 1e12, 2),
-        "flop_count": "value counts 38*B*H*N^2*d (the paper's 19 tile contractions per Alg. 2); this build executes "
-                      "36 (Pass 1 takes dQ and skips R); bob_tflops_executed uses 36, bob_tflops_min_count 24",
+        "flop_count": f"value counts 38*B*H*{nsq}*d (the paper's 19 tile contractions per Alg. 2); this build "
+                      f"executes 36 (Pass 1 takes dQ and skips R); bob_tflops_executed uses 36, "
+                      f"bob_tflops_min_count 24",
         "step_tflops": round(step_flops / (wall / args.steps) / 1e12, 2),
         "kernels": kern,
         "peak_mem_gib": round(torch.cuda.max_memory_allocated(dev) / 2**30, 3),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic},
     }
+    if w.causal:
+        line["metric"] = line["metric"].replace("N^2", "N(N+1)/2")
+    pn = peak_n_summary()
+    if pn is not None:
+        line["peak_n"] = pn
+    if w.causal and (w.B, w.H, w.d) == (4, 12, 64) and w.N in PAPER_TABLE1_MS:
+        ref = PAPER_TABLE1_MS[w.N]
+        line["paper_context"] = {
+            "source": "Table 1: one A100 80GB, Triton, causal B=4 H=12 d=64 bf16; scope of the timing unstated",
+            "paper_ms": ref, "this_bob_ms": round(bob_med, 3), "this_step_ms": round(wall / args.steps * 1e3, 3),
+            "bob_speedup": round(ref / bob_med, 2), "step_speedup": round(ref / (wall / args.steps * 1e3), 2)}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle for about {args.cpu_seconds} s")
         line["cpu_baseline"] = cpu_baseline(x_cpu, w, budget_s=args.cpu_seconds)

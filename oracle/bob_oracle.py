@@ -277,8 +277,8 @@ def bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal=False):
     """Row-owned outputs of one head restricted to the query rows `rows`.
 
     Every row-owned quantity (Qt, dOt, alpha, E, O, L, D, dQ) of row i depends
-    only on row i of the N x N matrices (Sec. 3.2: they "sum over columns for
-    each fixed row"), so the same definitions applied to a slab of query rows
+    only on row i of the N x N matrices (Sec. 3.2: each is a sum over the
+    columns of one fixed row), so the same definitions applied to a slab of query rows
     give exactly those rows.  Used for large N, where the full N x N matrices
     do not fit.
     """
@@ -322,8 +322,8 @@ def bob_cols(q, k, v, do, uq, uk, uv, tau, cols, alpha, E, L, D, causal=False):
     """Column-owned outputs of one head (Kt, Vt, and the producer's dK, dV) at
     the key rows `cols`.
 
-    Column j sums over every query row i (Sec. 3.2: Kt and Vt "sum over rows
-    for each fixed column"), so the row scalars alpha, E, L, D of all rows are
+    Column j sums over every query row i (Sec. 3.2: Kt and Vt are sums over
+    the rows of one fixed column), so the row scalars alpha, E, L, D of all rows are
     inputs here; callers compute them with row_scalars() from this module.
     The per-tile quantities follow the same definitions as bob_head, taken on
     the N x |cols| slice of the attention matrices.

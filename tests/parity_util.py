@@ -74,3 +74,45 @@ def global_identities(x, out):
         t = out[name].double().flatten(0, 1)                 # [B*H, N, d]
         colsum[name] = float((t.sum(1).norm(dim=-1) / t.norm(dim=(1, 2))).max())
     return scal, colsum
+
+
+ROW_KEYS = ("Qt", "dOt", "alpha", "E", "O", "L", "D", "dQ")
+SCALAR_TOL = 5e-3     # |lhs - rhs| / scale for I1-I3
+COLSUM_TOL = 1e-2     # ||sum_j X_j|| / ||X||_F for I5, I6
+
+
+def check_rows(x, out, w, rows_per_head, seed, slab=64, causal=False, keys=ROW_KEYS):
+    """Row-owned outputs of the GPU path on `rows_per_head` sampled query rows
+    of every head against the oracle's `bob_rows` on the same rows (under the
+    causal mask row 0, which sees a single key, is always included)."""
+    rng = np.random.default_rng(seed)
+    got = {k: [] for k in keys}
+    want = {k: [] for k in keys}
+    for b in range(w.B):
+        for h in range(w.H):
+            mats = [as_f64(x[n][b, h]) for n in NAMES]
+            rows = rng.choice(w.N, size=rows_per_head, replace=False)
+            if causal:
+                rows[0] = 0
+            rows = np.unique(rows)
+            for r0 in range(0, len(rows), slab):
+                sel = rows[r0:r0 + slab]
+                ref = oracle.bob_rows(*mats, w.scale, sel, causal=causal)
+                idx = torch.as_tensor(sel, device=out["Qt"].device)
+                for k in keys:
+                    got[k].append(as_f64(out[k][b, h].index_select(0, idx)))
+                    want[k].append(ref[k])
+    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in keys}
+    say("   sampled-row errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL["bf16"], (k, e)
+
+
+def check_identities(x, out):
+    scal, colsum = global_identities(x, out)
+    say("   identities", {k: f"{(a - b) / s:.2e}" for k, (a, b, s) in scal.items()},
+        {k: f"{v:.2e}" for k, v in colsum.items()})
+    for k, (a, b, s) in scal.items():
+        assert abs(a - b) <= SCALAR_TOL * s, k
+    for k, v in colsum.items():
+        assert v <= COLSUM_TOL, k

@@ -2,13 +2,15 @@
 the float64 oracle with the same mask: every output element at small and
 ragged sizes (tiles skipped above the diagonal, diagonal tiles masked per
 element), both Pass 1 forms, both dtypes and head dims; and sampled rows plus
-global identities at N = 16384, d = 128."""
+global identities at N = 16384, d = 128 and at the causal benchmark workload
+(B=4, H=12, N=16384, d=64)."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from tests.parity_util import TOL, global_identities, nrel, oracle_full, run_gpu_path, say, to_dev
+from tests.parity_util import (TOL, check_identities, check_rows, nrel, oracle_full, run_gpu_path, say,
+                               to_dev)
 from workloads import NAMES, WORKLOADS, as_f64, make_inputs, workload_inputs
 
 pytestmark = pytest.mark.gpu
@@ -55,30 +57,22 @@ def test_causal_full_path_matches_oracle(case):
 
 def test_causal_n16384_d128_sampled_rows_and_identities():
     w = WORKLOADS["bf16_b1h16_n16384_d128"]
+    say(f"[causal] {w.name} under the causal mask: GPU path")
+    x = workload_inputs(w)
+    xd = to_dev(x)
+    out = run_gpu_path(xd, w.scale, causal=True)
+    check_rows(x, out, w, rows_per_head=32, seed=5005, causal=True)
+    check_identities(xd, out)
+
+
+@pytest.mark.parametrize("name", ["causal_bf16_b4h12_n16384_d64"])
+def test_causal_paper_shape_sampled_rows_and_identities(name):
+    """The causal benchmark workload (the paper's kernel shape), in the launch
+    configuration the benchmark times."""
+    w = WORKLOADS[name]
     say(f"[causal] {w.name}: GPU path")
     x = workload_inputs(w)
     xd = to_dev(x)
     out = run_gpu_path(xd, w.scale, causal=True)
-    rng = np.random.default_rng(5005)
-    got, want = {k: [] for k in ("Qt", "dOt", "alpha", "E", "L", "D")}, {k: [] for k in ("Qt", "dOt", "alpha", "E", "L", "D")}
-    for h in range(w.H):
-        mats = [as_f64(x[n][0, h]) for n in NAMES]
-        rows = np.sort(rng.choice(w.N, size=32, replace=False))
-        rows[0] = 0                                     # the single-key row
-        rows = np.unique(rows)
-        ref = oracle.bob_rows(*mats, w.scale, rows, causal=True)
-        idx = torch.as_tensor(rows, device=out["Qt"].device)
-        for k in got:
-            got[k].append(as_f64(out[k][0, h].index_select(0, idx)))
-            want[k].append(ref[k])
-    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in got}
-    say("   sampled-row errs", {k: f"{v:.2e}" for k, v in errs.items()})
-    for k, e in errs.items():
-        assert e <= TOL["bf16"], (k, e)
-    scal, colsum = global_identities(xd, out)
-    say("   identities", {k: f"{(a - b) / s:.2e}" for k, (a, b, s) in scal.items()},
-        {k: f"{v:.2e}" for k, v in colsum.items()})
-    for k, (a, b, s) in scal.items():
-        assert abs(a - b) <= 5e-3 * s, k
-    for k, v in colsum.items():
-        assert v <= 1e-2, k
+    check_rows(x, out, w, rows_per_head=8, seed=5006, causal=True)
+    check_identities(xd, out)

@@ -16,46 +16,10 @@ import pytest
 import torch
 
 import oracle
-from tests.parity_util import TOL, global_identities, lib, nrel, run_gpu_path, say, to_dev
+from tests.parity_util import TOL, check_identities, check_rows, lib, nrel, run_gpu_path, say, to_dev
 from workloads import NAMES, WORKLOADS, as_f64, workload_inputs
 
 pytestmark = pytest.mark.gpu
-
-ROW_KEYS = ("Qt", "dOt", "alpha", "E", "O", "L", "D", "dQ")
-SCALAR_TOL = 5e-3     # |lhs - rhs| / scale for I1-I3
-COLSUM_TOL = 1e-2     # ||sum_j X_j|| / ||X||_F for I5, I6
-
-
-def check_rows(x, out, w, rows_per_head, seed, slab=64):
-    rng = np.random.default_rng(seed)
-    got = {k: [] for k in ROW_KEYS}
-    want = {k: [] for k in ROW_KEYS}
-    for b in range(w.B):
-        for h in range(w.H):
-            mats = [as_f64(x[n][b, h]) for n in NAMES]
-            rows = np.sort(rng.choice(w.N, size=rows_per_head, replace=False))
-            for r0 in range(0, len(rows), slab):
-                sel = rows[r0:r0 + slab]
-                ref = oracle.bob_rows(*mats, w.scale, sel)
-                idx = torch.as_tensor(sel, device=out["Qt"].device)
-                for k in ROW_KEYS:
-                    got[k].append(as_f64(out[k][b, h].index_select(0, idx)))
-                    want[k].append(ref[k])
-    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in ROW_KEYS}
-    say("   sampled-row errs", {k: f"{v:.2e}" for k, v in errs.items()})
-    for k, e in errs.items():
-        assert e <= TOL["bf16"], (k, e)
-
-
-def check_identities(x, out):
-    scal, colsum = global_identities(x, out)
-    say("   identities", {k: f"{(a - b) / s:.2e}" for k, (a, b, s) in scal.items()},
-        {k: f"{v:.2e}" for k, v in colsum.items()})
-    for k, (a, b, s) in scal.items():
-        assert abs(a - b) <= SCALAR_TOL * s, k
-    for k, v in colsum.items():
-        assert v <= COLSUM_TOL, k
-
 
 def test_n16384_d128():
     w = WORKLOADS["bf16_b1h16_n16384_d128"]

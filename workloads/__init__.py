@@ -29,6 +29,7 @@ class Workload:
     dtype: str          # "f32" or "bf16"
     seed: int
     qk_scale: float = 1.0
+    causal: bool = False  # the problem flag passed with these inputs (not part of the draw)
 
     @property
     def scale(self) -> float:
@@ -39,14 +40,20 @@ class Workload:
         return torch.float32 if self.dtype == "f32" else torch.bfloat16
 
 
-# The five workloads: a tiny fp32 case, a small bf16 case, the N=16K d=128
-# case, a long-context N=64K case and the N=256K maximum-length case.
+# The five dense workloads: a tiny fp32 case, a small bf16 case, the N=16K
+# d=128 case, a long-context N=64K case and the N=256K maximum-length case.
+# Two causal workloads follow at the shape of the paper's own kernel timings
+# (causal, B=4, H=12, d=64; Table 1), for comparison with those figures.
 WORKLOADS = {
     "tiny_f32_n256_d64": Workload("tiny_f32_n256_d64", 1, 1, 256, 64, "f32", 0),
     "bf16_b2h8_n4096_d64": Workload("bf16_b2h8_n4096_d64", 2, 8, 4096, 64, "bf16", 1),
     "bf16_b1h16_n16384_d128": Workload("bf16_b1h16_n16384_d128", 1, 16, 16384, 128, "bf16", 2, 0.5),
     "bf16_b1h8_n65536_d64": Workload("bf16_b1h8_n65536_d64", 1, 8, 65536, 64, "bf16", 3),
     "bf16_b1h4_n262144_d64": Workload("bf16_b1h4_n262144_d64", 1, 4, 262144, 64, "bf16", 4),
+    "causal_bf16_b4h12_n16384_d64": Workload("causal_bf16_b4h12_n16384_d64", 4, 12, 16384, 64, "bf16", 5,
+                                             causal=True),
+    "causal_bf16_b4h12_n65536_d64": Workload("causal_bf16_b4h12_n65536_d64", 4, 12, 65536, 64, "bf16", 6,
+                                             causal=True),
 }
 
 
