@@ -272,24 +272,50 @@ __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, i
 // fetches the logical chunk that belongs at that (permuted) position.  Rows
 // >= N are clamped to row N-1 (finite data); every kernel masks them out.
 // The copy is asynchronous: wait_vm<>() before the barrier that publishes it.
+// Loads each wave issues per streamed tile: the NTENS x kBlocks 1 KB blocks
+// of one tile stage are dealt out evenly over the NW waves.
+template <typename T, int D, int NW, int NTENS>
+constexpr int tile_loads() {
+  static_assert((NTENS * Geo<T, D>::kBlocks) % NW == 0, "tile blocks per wave");
+  return NTENS * Geo<T, D>::kBlocks / NW;
+}
+
 template <typename T, int D, int NW, int NTENS>
 __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N) {
   using G = Geo<T, D>;
-  static_assert(G::kBlocks % NW == 0, "tile blocks per wave");
+  constexpr int kBlockElems = 1024 / (int)sizeof(T);
   const int l = lane_id(), w = wave_id();
-#pragma unroll
-  for (int bi = 0; bi < G::kBlocks / NW; ++bi) {
-    const int b = w + bi * NW;
+  auto one = [&](const T* base, int t, int b) {
     const int q = b * 64 + l;
     const int r = q / G::kCPR;
     const int c = G::logical(r, q % G::kCPR);
     const int row = min(s0 + r, N - 1);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(base + (int64_t)row * D + c * G::kEPC),
+        (__attribute__((address_space(3))) void*)(dst + t * G::kTileElems + b * kBlockElems), 16, 0, 0);
+  };
+  if constexpr (G::kBlocks % NW == 0) {
+    // every wave takes the same block positions of every tensor
 #pragma unroll
-    for (int t = 0; t < NTENS; ++t)
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(src[t] + (int64_t)row * D + c * G::kEPC),
-          (__attribute__((address_space(3))) void*)(dst + t * G::kTileElems + b * (1024 / (int)sizeof(T))),
-          16, 0, 0);
+    for (int bi = 0; bi < G::kBlocks / NW; ++bi)
+#pragma unroll
+      for (int t = 0; t < NTENS; ++t) one(src[t], t, w + bi * NW);
+  } else {
+    // more waves than blocks per tensor: kWPB waves share a block position
+    // and split the tensors between them (tensor index chosen by selects,
+    // not by indexing the pointer array, which would go through scratch)
+    constexpr int kWPB = NW / G::kBlocks;
+    static_assert(NW % G::kBlocks == 0 && NTENS % kWPB == 0, "tile blocks per wave");
+    const int b = w % G::kBlocks, t0 = w / G::kBlocks;
+#pragma unroll
+    for (int i = 0; i < NTENS / kWPB; ++i) {
+      const int t = t0 + i * kWPB;
+      const T* base = src[0];
+#pragma unroll
+      for (int u = 1; u < NTENS; ++u)
+        if (t == u) base = src[u];
+      one(base, t, b);
+    }
   }
 }
 

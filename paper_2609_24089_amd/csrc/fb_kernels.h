@@ -84,7 +84,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
-  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       0, it_end,
       [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
@@ -194,7 +194,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
   const T* const src[2] = {K + hoff, V + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
-  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       0, it_end,
       [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   const T* const src[2] = {Q + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
-  stream_loop<NSTAGE, 2 * (G::kBlocks / NW)>(
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       it_begin, nT,
       [&](int it, int st) {
         if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);
@@ -513,7 +513,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
-  stream_loop<NSTAGE, 4 * (G::kBlocks / NW)>(
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 4>()>(
       0, it_end,
       [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
@@ -634,7 +634,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
-  stream_loop<NSTAGE, 3 * (G::kBlocks / NW)>(
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 3>()>(
       it_begin, nT,
       [&](int it, int st) {
         if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);

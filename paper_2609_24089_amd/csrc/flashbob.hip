@@ -18,11 +18,11 @@ struct Shape {
 };
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 64> {
-  static constexpr Shape kFwd{2, 4, 1, 2}, kRows{2, 4, 1, 2}, kCols{2, 4, 1, 2};
-  static constexpr Shape kP1{2, 4, 1, 2}, kP1Six{2, 4, 1, 2}, kP2{2, 4, 2, 3};
+  static constexpr Shape kFwd{1, 8, 2, 2}, kRows{1, 8, 2, 2}, kCols{1, 8, 2, 2};
+  static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 3};
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr Shape kFwd{2, 4, 1, 2}, kRows{2, 4, 1, 2}, kCols{2, 4, 1, 2};
+  static constexpr Shape kFwd{1, 8, 2, 3}, kRows{1, 4, 2, 2}, kCols{1, 4, 2, 2};
   static constexpr Shape kP1{1, 8, 2, 3}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 3};
 };
 template <> struct Cfg<float, 64> {
