@@ -181,3 +181,6 @@ def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, use_dq=True, stream=Non
                                             dQ=dQ if use_dq else None, stream=stream)
     Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)
+
+
+from .autograd import attention  # noqa: E402  (differentiable wrapper; imports the entry points above)

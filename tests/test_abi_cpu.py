@@ -118,3 +118,12 @@ def test_binding_rejects_cpu_tensors():
         fb.attn_fwd_lse(x, x, x, 0.125)
     with pytest.raises(TypeError):
         fb._dtype_code(torch.zeros(1, dtype=torch.float16))
+
+
+def test_attention_wrapper_rejects_host_tensors():
+    """The differentiable wrapper has no host path: CPU tensors are refused
+    before any library call."""
+    import torch
+    x = torch.zeros(1, 1, 8, 64)
+    with pytest.raises(ValueError, match="ROCm device"):
+        fb.attention(x, x, x)
