@@ -15,6 +15,7 @@ counts use the N(N+1)/2 unmasked (query, key) pairs per head instead of N^2.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --peak-n     # longest N (B=H=1, d=64) under a 60 s BoB cap
+    python bench.py --ablation --workload NAME   # two- vs three-pass schedule
 """
 import argparse
 import hashlib
@@ -241,6 +242,57 @@ def peak_n_sweep(args, log):
     print(json.dumps(line), flush=True)
 
 
+def ablation(args, log):
+    """The schedule ablation (App. "Three-pass versus two-pass", Table 7): on
+    one workload, the median time of the BoB passes under (a) the two-pass
+    schedule as this build runs it (Pass 1 with dQ), (b) the two-pass schedule
+    with the six accumulators of Prop. 3.1 and (c) the three-pass control
+    schedule (alpha sweep, row sweep, column pass).  Interleaved repetitions
+    on the same resident inputs; prints one JSON line."""
+    import torch
+    import paper_2609_24089_amd as fb
+    from workloads import WORKLOADS, workload_inputs
+    fb.load_library()
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    x = {k: v.to(dev) for k, v in workload_inputs(w).items()}
+    Q, K, V, dO, UQ, UK, UV = (x[n] for n in ("Q", "K", "V", "dO", "UQ", "UK", "UV"))
+    s, c = w.scale, w.causal
+    O, L = fb.attn_fwd_lse(Q, K, V, s, causal=c)
+    dQ, dK, dV, D = fb.attn_bwd(Q, K, V, O, dO, L, s, causal=c)
+    E_ = lambda: torch.empty_like(Q)
+    R_ = lambda: torch.empty((w.B, w.H, w.N), dtype=torch.float32, device=dev)
+    o1, o2, al3, o3 = (E_(), E_(), R_(), R_()), (E_(), E_()), R_(), (E_(), E_(), R_())
+    runs = {
+        "two_pass_dq": lambda: (fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, s, causal=c, dQ=dQ, out=o1),
+                                fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, o1[2], o1[3], s, causal=c, out=o2)),
+        "two_pass_six": lambda: (fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, s, causal=c, out=o1),
+                                 fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, o1[2], o1[3], s, causal=c, out=o2)),
+        "three_pass": lambda: (fb.attn_bob3_alpha_rows(Q, K, UQ, UK, L, s, causal=c, out=al3),
+                               fb.attn_bob3_rows(Q, K, V, dO, UQ, UK, UV, L, D, al3, s, causal=c, out=o3),
+                               fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al3, o3[2], s, causal=c, out=o2)),
+    }
+    times = {k: [] for k in runs}
+    for rep in range(args.warmup + args.steps):
+        for k, fn in runs.items():
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize(dev)
+            if rep >= args.warmup:
+                times[k].append(e0.elapsed_time(e1))
+    med = {k: statistics.median(v) for k, v in times.items()}
+    log(f"ablation {w.name}: " + ", ".join(f"{k} {v:.3f} ms" for k, v in med.items()))
+    line = {"metric": "BoB time by schedule (median ms of the BoB passes; ratio = schedule / two_pass_six)",
+            "workload": w.name, "causal": w.causal, "steps": args.steps, "warmup": args.warmup,
+            "ms": {k: round(v, 4) for k, v in med.items()},
+            "ratio_vs_two_pass_six": {k: round(v / med["two_pass_six"], 4) for k, v in med.items()},
+            "ratio_three_over_two_dq": round(med["three_pass"] / med["two_pass_dq"], 4),
+            "paper_context": "Table 7 (A100, causal B=4 H=12 d=64): three-pass / two-pass = 1.05-1.07"}
+    print(json.dumps(line), flush=True)
+
+
 def peak_n_summary():
     """The committed peak-N sweep, if it was taken on the current kernels."""
     try:
@@ -265,6 +317,8 @@ def main():
     ap.add_argument("--peak-n", action="store_true", help="run the peak-N sweep instead of the step benchmark")
     ap.add_argument("--peak-n-start", type=int, default=1 << 18)
     ap.add_argument("--peak-n-cap", type=float, default=60.0)
+    ap.add_argument("--ablation", action="store_true",
+                    help="time the two-pass and three-pass schedules on --workload instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -274,6 +328,9 @@ def main():
     log = lambda msg: print(f"[bench] {msg}", file=sys.stderr, flush=True)
     if args.peak_n:
         peak_n_sweep(args, log)
+        return
+    if args.ablation:
+        ablation(args, log)
         return
 
     import torch

@@ -106,6 +106,31 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
                             const float* L, const float* D, const float* alpha, const float* E,
                             void* Kt, void* Vt, void* stream);
 
+/* Three-pass control schedule (App. "Three-pass versus two-pass" and the
+ * three-pass overlay of App. "Dependency graphs"): the schedule that the
+ * affine fusion of Prop. 3.1 improves on, kept for the 2- vs 3-pass ablation
+ * (Table 7).  Sweep 1 is attn_bob3_alpha_rows, sweep 2 attn_bob3_rows, sweep 3
+ * the shared column pass attn_bob_pass2_cols.  The results equal those of
+ * attn_bob_pass1_rows up to rounding.
+ *
+ * Sweep 1, row-major: alpha_i = sum_j P_ij F_ij alone (F = scale (U_Q K^T +
+ * Q U_K^T)), streaming only K and U_K.
+ * In:  Q, K, gdQ (= U_Q), gdK (= U_K) [B,H,N,d];  L fp32 [B,H,N].
+ * Out: alpha fp32 [B,H,N]. */
+int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                             int32_t causal, const void* Q, const void* K, const void* gdQ, const void* gdK,
+                             const float* L, float* alpha, void* stream);
+
+/* Sweep 2, row-major, with alpha from sweep 1: forms Pt = C + F (dP - D) -
+ * alpha dP and h = F - alpha directly and applies one delayed correction,
+ * Qt = scale (sum_j P Pt k_j + dS U_K - E sum_j P k_j), dOt = P U_V + (P h) V.
+ * In:  Q, K, V, dO, gdQ, gdK, gdV [B,H,N,d];  L, D, alpha fp32 [B,H,N].
+ * Out: Qt, dOt [B,H,N,d];  E fp32 [B,H,N]. */
+int32_t attn_bob3_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
+                       const void* Q, const void* K, const void* V, const void* dO, const void* gdQ,
+                       const void* gdK, const void* gdV, const float* L, const float* D, const float* alpha,
+                       void* Qt, void* dOt, float* E, void* stream);
+
 /* 1 if (dtype, d) is built into this library, else 0. */
 int32_t bob_supported(int32_t dtype, int64_t d);
 

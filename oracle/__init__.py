@@ -8,13 +8,15 @@ library and never consumes a value produced by it.
 Every function takes plain NumPy arrays, works in float64 and materialises
 the full (or row-slab) N x N attention matrices, following the paper's
 definitions directly (Sec. 2 eqs. 1-3, Sec. 3.1 eqs. 4-5, Sec. 3.2 eqs. 6-8,
-App. A "Final assembled identities", App. B proof of Prop. 3.1).
+App. A "Final assembled identities", App. B proof of Prop. 3.1, and the three-pass control schedule of App.
+"Three-pass versus two-pass").
 """
 from .bob_oracle import (  # noqa: F401
     forward_head,
     first_backward_head,
     bob_head,
     bob_affine_head,
+    bob_threepass_head,
     first_backward_rowloop,
     phi_rowloop,
     forward,
@@ -22,6 +24,7 @@ from .bob_oracle import (  # noqa: F401
     bob,
     bob_rows,
     bob_affine,
+    bob_threepass,
     row_scalars,
     bob_cols,
 )

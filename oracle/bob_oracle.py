@@ -191,6 +191,37 @@ def bob_affine_head(q, k, v, do, uq, uk, uv, tau, causal=False):
     return dict(Qt=Qt, dOt=dOt, alpha=alpha, E=E, E0=E0)
 
 
+def bob_threepass_head(q, k, v, do, uq, uk, uv, tau, causal=False):
+    """Row-owned outputs through the three-pass control schedule (App.
+    "Three-pass versus two-pass"; the three-pass overlay figure of App.
+    "Dependency graphs").
+
+    Its first sweep forms only alpha = sum_j P F.  Its second sweep, with
+    alpha known, forms Pt = C + F (dP - D) - alpha dP and h = F - alpha
+    directly and keeps one delayed correction: it accumulates
+    E = sum_j P Pt, Omega' = (P Pt) K + dS U_K and B = P K, then
+    Qt = tau (Omega' - E B) because S~ = P (Pt - E); dOt = P U_V + (P h) V.
+    (Its third sweep is the column pass shared with the two-pass schedule.)
+    Whole rows at once: a further route to the same numbers, not a tiling.
+    """
+    O, L, P, _ = forward_head(q, k, v, tau, causal)
+    dP = dP_of(do, v)
+    D = row_D(P, dP)
+    F = F_of(q, k, uq, uk, tau)
+    C = C_of(do, uv)
+    # sweep 1
+    alpha = (P * F).sum(axis=-1)
+    # sweep 2
+    Pt = C + F * (dP - D[:, None]) - alpha[:, None] * dP
+    h = F - alpha[:, None]
+    E = (P * Pt).sum(axis=-1)
+    OmegaP = (P * Pt) @ k + (P * (dP - D[:, None])) @ uk
+    Bacc = P @ k
+    Qt = tau * (OmegaP - E[:, None] * Bacc)
+    dOt = P @ uv + (P * h) @ v
+    return dict(Qt=Qt, dOt=dOt, alpha=alpha, E=E)
+
+
 # --------------------------------------------------------------------------
 # An independently written first backward g(Q, K, V, dO) = (dQ, dK, dV):
 # one query row at a time, the softmax Jacobian written out as
@@ -265,6 +296,12 @@ def bob(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
     """Batched BoB (eqs. 6-7): dict(Qt, Kt, Vt, dOt, alpha, E, O, L, D, dQ, dK, dV)."""
     keys = ("Qt", "Kt", "Vt", "dOt", "alpha", "E", "O", "L", "D", "dQ", "dK", "dV")
     return _batched(bob_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau, causal=causal)
+
+
+def bob_threepass(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
+    """Batched three-pass control route: dict(Qt, dOt, alpha, E)."""
+    keys = ("Qt", "dOt", "alpha", "E")
+    return _batched(bob_threepass_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau, causal=causal)
 
 
 def bob_affine(Q, K, V, dO, UQ, UK, UV, tau, causal=False):

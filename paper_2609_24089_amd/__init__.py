@@ -37,7 +37,10 @@ def load_library():
     lib.attn_bwd.argtypes = common + [vp] * 10 + [vp]
     lib.attn_bob_pass1_rows.argtypes = common + [vp] * 15 + [vp]
     lib.attn_bob_pass2_cols.argtypes = common + [vp] * 13 + [vp]
-    for fn in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"):
+    lib.attn_bob3_alpha_rows.argtypes = common + [vp] * 6 + [vp]
+    lib.attn_bob3_rows.argtypes = common + [vp] * 13 + [vp]
+    for fn in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols",
+               "attn_bob3_alpha_rows", "attn_bob3_rows"):
         getattr(lib, fn).restype = i32
     lib.bob_supported.argtypes = [i32, i64]
     lib.bob_supported.restype = i32
@@ -164,6 +167,46 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
           _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
           _p(Kt), _p(Vt), _stream(stream))
     return Kt, Vt
+
+
+def attn_bob3_alpha_rows(Q, K, gdQ, gdK, L, scale, causal=False, out=None, stream=None):
+    """Three-pass control schedule, sweep 1: returns alpha."""
+    B, H, N, d = _check_mats(Q, K, gdQ, gdK)
+    _check_rows(Q.shape, L)
+    alpha = _rows_empty(Q.shape, Q) if out is None else out
+    _check_rows(Q.shape, alpha)
+    lib = load_library()
+    _call(lib.attn_bob3_alpha_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
+          _p(Q), _p(K), _p(gdQ), _p(gdK), _p(L), _p(alpha), _stream(stream))
+    return alpha
+
+
+def attn_bob3_rows(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, scale, causal=False, out=None, stream=None):
+    """Three-pass control schedule, sweep 2: returns (Qt, dOt, E)."""
+    B, H, N, d = _check_mats(Q, K, V, dO, gdQ, gdK, gdV)
+    _check_rows(Q.shape, L, D, alpha)
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q))
+    Qt, dOt, E = out
+    _check_mats(Q, Qt, dOt)
+    _check_rows(Q.shape, E)
+    lib = load_library()
+    _call(lib.attn_bob3_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
+          _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha),
+          _p(Qt), _p(dOt), _p(E), _stream(stream))
+    return Qt, dOt, E
+
+
+def bob3(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, stream=None):
+    """Whole path with the three-pass control schedule: forward, first
+    backward, sweep 1 (alpha), sweep 2 (Qt, dOt, E), sweep 3 (Kt, Vt).
+    Returns the same dict as bob()."""
+    O, L = attn_fwd_lse(Q, K, V, scale, causal, stream=stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream)
+    alpha = attn_bob3_alpha_rows(Q, K, gdQ, gdK, L, scale, causal, stream=stream)
+    Qt, dOt, E = attn_bob3_rows(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, scale, causal, stream=stream)
+    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream)
+    return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)
 
 
 def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, use_dq=True, stream=None):

@@ -377,22 +377,33 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
 // Epilogue (eq. 8): E = E0 - alpha D, dOt = dOt0 - alpha O,
 // Qt = tau (Omega - alpha R - E Bacc).  Writes alpha, E, Qt, dOt once.
 //
-// kDQ variant: when the first-backward dQ is supplied, R is not accumulated.
+// kWithDQ form: when the first-backward dQ is supplied, R is not accumulated.
 // Since dQ / tau = sum_j P (dP - D) k_j = R - D Bacc, eq. 8 becomes
 // Qt = tau (Omega - E0 Bacc) - alpha dQ with E0 = E + alpha D.  This drops one
 // B_r x d accumulator and one tile contraction per tile, which is what lets
 // the d = 128 kernel run two waves per SIMD.
+//
+// kAlphaGiven form: the second sweep of the three-pass control schedule
+// (App. "Three-pass versus two-pass").  alpha comes in from a first sweep, so
+// Pt = C + F (dP - D) - alpha dP and h = F - alpha are formed directly; the
+// kernel accumulates E += rowsum(P Pt), Omega' += (P Pt) K + (P (dP - D)) U_K,
+// Bacc += P K, dOt += P U_V + (P h) V and finishes Qt = tau (Omega' - E Bacc)
+// (the one delayed correction).  Writes E, Qt, dOt.
 // ===========================================================================
-template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, bool kDQ>
+enum Pass1Form : int { kSixAcc = 0, kWithDQ = 1, kAlphaGiven = 2 };
+
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
     const T* __restrict__ UK, const T* __restrict__ UV, const float* __restrict__ L,
-    const float* __restrict__ Dv, const T* __restrict__ dQ, T* __restrict__ Qt, T* __restrict__ dOt,
-    float* __restrict__ alpha_out, float* __restrict__ E_out, int N, int nRB, int total, float scale,
-    int causal) {
+    const float* __restrict__ Dv, const T* __restrict__ dQ, const float* __restrict__ alpha_in,
+    T* __restrict__ Qt, T* __restrict__ dOt, float* __restrict__ alpha_out, float* __restrict__ E_out,
+    int N, int nRB, int total, float scale, int causal) {
   using E = Elt<T>;
   using G = Geo<T, D>;
+  constexpr bool kDQ = kForm == kWithDQ;
+  constexpr bool kThree = kForm == kAlphaGiven;
   constexpr int BR = 16 * MR * NW;
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][4 * G::kTileElems];
 
@@ -404,7 +415,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   const int row0 = rb * BR + wave_id() * 16 * MR;
 
   u32x4 qf[MR][G::kChunks], uqf[MR][G::kChunks], dof[MR][G::kChunks];
-  float lb[MR], drow[MR];
+  float lb[MR], drow[MR], arow[MR];
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
     const int row = row0 + 16 * mb + j;
@@ -413,8 +424,9 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     load_stationary<T, D>(dof[mb], dO + hoff, row, N);
     lb[mb] = row < N ? L[soff + row] * kLog2e : 0.f;
     drow[mb] = row < N ? Dv[soff + row] : 0.f;
+    arow[mb] = (kThree && row < N) ? alpha_in[soff + row] : 0.f;
   }
-  constexpr int kNR = kDQ ? 1 : G::kNB;  // R accumulator only in the six-accumulator form
+  constexpr int kNR = (kForm == kSixAcc) ? G::kNB : 1;  // R accumulator only in the six-accumulator form
   floatx4 aDO[G::kNB][MR], aOM[G::kNB][MR], aB[G::kNB][MR], aR[kNR][MR];
 #pragma unroll
   for (int nb = 0; nb < G::kNB; ++nb)
@@ -473,17 +485,26 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           const float fv = f[sb][mb][r] * scale;
           const float dpv = dp[sb][mb][r];
           const float dd = dpv - drow[mb];
-          const float pt0 = __builtin_fmaf(fv, dd, cc[sb][mb][r]);
-          const float pf = p * fv;
-          const float ppt = p * pt0;
-          alpha[mb] += pf;
-          e0[mb] += ppt;
           const int i = 4 * sb + r;
+          if constexpr (kThree) {
+            // Pt with alpha known; fPF carries P h (h = F - alpha) here
+            const float pt = __builtin_fmaf(-arow[mb], dpv, __builtin_fmaf(fv, dd, cc[sb][mb][r]));
+            const float ppt = p * pt;
+            e0[mb] += ppt;
+            fPF[mb].set(i, p * (fv - arow[mb]));
+            fPPt[mb].set(i, ppt);
+          } else {
+            const float pt0 = __builtin_fmaf(fv, dd, cc[sb][mb][r]);
+            const float pf = p * fv;
+            const float ppt = p * pt0;
+            alpha[mb] += pf;
+            e0[mb] += ppt;
+            fPF[mb].set(i, pf);
+            fPPt[mb].set(i, ppt);
+          }
           fP[mb].set(i, p);
-          fPF[mb].set(i, pf);
-          fPPt[mb].set(i, ppt);
           fPdd[mb].set(i, p * dd);
-          if (!kDQ) fPdp[mb].set(i, p * dpv);
+          if constexpr (kForm == kSixAcc) fPdp[mb].set(i, p * dpv);
         }
     }
   };
@@ -501,7 +522,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) {
         aB[nb][mb] = E::mma_acc(ak, fP[mb], aB[nb][mb]);
-        if (!kDQ) aR[nb][mb] = E::mma_acc(ak, fPdp[mb], aR[nb][mb]);
+        if constexpr (kForm == kSixAcc) aR[nb][mb] = E::mma_acc(ak, fPdp[mb], aR[nb][mb]);
         aOM[nb][mb] = E::mma_acc(ak, fPPt[mb], aOM[nb][mb]);
         aOM[nb][mb] = E::mma_acc(auk, fPdd[mb], aOM[nb][mb]);
         aDO[nb][mb] = E::mma_acc(auv, fP[mb], aDO[nb][mb]);
@@ -533,10 +554,23 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         accumulate(Ks);
       });
 
-  // epilogue (eq. 8)
+  // epilogue (eq. 8; for kAlphaGiven the delayed E correction alone)
 #pragma unroll
   for (int mb = 0; mb < MR; ++mb) {
     const int row = row0 + 16 * mb + j;
+    if constexpr (kThree) {
+      const float ee = group_sum(e0[mb]);
+      if (row < N) {
+        if (g == 0) E_out[soff + row] = ee;
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const int64_t off = hoff + (int64_t)row * D + 16 * nb + 4 * g;
+          E::store4(dOt + off, aDO[nb][mb]);
+          E::store4(Qt + off, scale * (aOM[nb][mb] - ee * aB[nb][mb]));
+        }
+      }
+      continue;
+    }
     const float al = group_sum(alpha[mb]);
     const float e0s = group_sum(e0[mb]);
     const float ee = e0s - al * drow[mb];
@@ -554,10 +588,100 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           const floatx4 dq = E::load4(dQ + off);
           E::store4(Qt + off, scale * (aOM[nb][mb] - e0s * aB[nb][mb]) - al * dq);
         } else {
-          E::store4(Qt + off, scale * (aOM[nb][mb] - al * aR[kDQ ? 0 : nb][mb] - ee * aB[nb][mb]));
+          E::store4(Qt + off, scale * (aOM[nb][mb] - al * aR[(kForm == kSixAcc) ? nb : 0][mb] - ee * aB[nb][mb]));
         }
       }
     }
+  }
+}
+
+// ===========================================================================
+// First sweep of the three-pass control schedule (App. "Three-pass versus
+// two-pass", the sweep that the affine fusion of Prop. 3.1 removes): row-major,
+// alpha_i = sum_j P_ij F_ij only.  Stationary: Q, U_Q rows.  Streamed: K, U_K
+// tiles.  Per tile: S^T = K Q^T, F^T = tau (K U_Q^T + U_K Q^T) and the row
+// sum of P F; no accumulate contractions.  Writes alpha once.
+// ===========================================================================
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
+__global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ UQ,
+    const T* __restrict__ UK, const float* __restrict__ L, float* __restrict__ alpha_out, int N, int nRB,
+    int total, float scale, int causal) {
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int BR = 16 * MR * NW;
+  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb, causal != 0);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t soff = (int64_t)bh * N;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  (void)l;
+  const int row0 = rb * BR + wave_id() * 16 * MR;
+
+  u32x4 qf[MR][G::kChunks], uqf[MR][G::kChunks];
+  float lb[MR], alpha[MR];
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    load_stationary<T, D>(qf[mb], Q + hoff, row, N);
+    load_stationary<T, D>(uqf[mb], UQ + hoff, row, N);
+    lb[mb] = row < N ? L[soff + row] * kLog2e : 0.f;
+    alpha[mb] = 0.f;
+  }
+  const float c = scale * kLog2e;
+  floatx4 s[2][MR], f[2][MR];
+
+  const T* const src[2] = {K + hoff, UK + hoff};
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
+      0, it_end,
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) {
+        const int s0 = it * kBS;
+        const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
+        if (mode == 0) return;
+        const T FB_LDS* Ks = (const T FB_LDS*)lds[st];
+        const T FB_LDS* UKs = Ks + G::kTileElems;
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb) s[sb][mb] = f[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int kk = 0; kk < G::kChunks; ++kk) {
+            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+            const u32x4 ak = *(const u32x4 FB_LDS*)(Ks + off);
+            const u32x4 auk = *(const u32x4 FB_LDS*)(UKs + off);
+#pragma unroll
+            for (int mb = 0; mb < MR; ++mb) {
+              s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);      // S^T = K Q^T
+              f[sb][mb] = E::mma_chunk(ak, uqf[mb][kk], f[sb][mb]);     // (U_Q K^T)^T
+              f[sb][mb] = E::mma_chunk(auk, qf[mb][kk], f[sb][mb]);     // + (Q U_K^T)^T
+            }
+          }
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s[sb][mb][r] = __builtin_fmaf(s[sb][mb][r], c, -lb[mb]);
+        if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
+#pragma unroll
+        for (int mb = 0; mb < MR; ++mb)
+#pragma unroll
+          for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) alpha[mb] = __builtin_fmaf(fast_exp2(s[sb][mb][r]), f[sb][mb][r], alpha[mb]);
+      });
+#pragma unroll
+  for (int mb = 0; mb < MR; ++mb) {
+    const int row = row0 + 16 * mb + j;
+    const float al = group_sum(alpha[mb]) * scale;
+    if (row < N && g == 0) alpha_out[soff + row] = al;
   }
 }
 

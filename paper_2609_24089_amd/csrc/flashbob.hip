@@ -20,18 +20,22 @@ template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{1, 8, 2, 2}, kRows{1, 8, 2, 2}, kCols{1, 8, 2, 2};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 3};
+  static constexpr Shape kAlpha{2, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{1, 8, 2, 3}, kRows{1, 4, 2, 2}, kCols{1, 4, 2, 2};
   static constexpr Shape kP1{1, 8, 2, 3}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 3};
+  static constexpr Shape kAlpha{2, 4, 2, 2};
 };
 template <> struct Cfg<float, 64> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
+  static constexpr Shape kAlpha{1, 4, 1, 2};
 };
 template <> struct Cfg<float, 128> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
+  static constexpr Shape kAlpha{1, 4, 1, 2};
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -122,18 +126,47 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   if (dQ != nullptr) {
     constexpr Shape c = Cfg<T, D>::kP1;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, true>), dim3(g.total),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ>), dim3(g.total),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
-                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
+                       (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
+                       p.causal);
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, false>), dim3(g.total),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc>), dim3(g.total),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
-                       (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
+                       (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
+                       p.causal);
   }
+  return finish_launch();
+}
+
+// Three-pass control schedule: the alpha-only sweep and the second row sweep.
+template <typename T, int D>
+int32_t launch_alpha3(const Problem& p, const void* Q, const void* K, const void* UQ, const void* UK,
+                      const float* L, float* alpha, hipStream_t s) {
+  constexpr Shape c = Cfg<T, D>::kAlpha;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((bob3_alpha_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)UQ, (const T*)UK, L, alpha, (int)p.N, g.nRB, g.total,
+                     p.scale, p.causal);
+  return finish_launch();
+}
+
+template <typename T, int D>
+int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
+                     const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
+                     const float* alpha, void* Qt, void* dOt, float* E, hipStream_t s) {
+  constexpr Shape c = Cfg<T, D>::kP1;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven>), dim3(g.total),
+                     dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)nullptr,
+                     (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr, alpha,
+                     (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
   return finish_launch();
 }
 
@@ -218,6 +251,32 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
   rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
   if (rc != BOB_OK) return rc;
   FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
+              (hipStream_t)stream);
+}
+
+int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
+                             int32_t causal, const void* Q, const void* K, const void* gdQ, const void* gdK,
+                             const float* L, float* alpha, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, gdQ, gdK, L, alpha});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_alpha3, p, Q, K, gdQ, gdK, L, alpha, (hipStream_t)stream);
+}
+
+int32_t attn_bob3_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
+                       const void* Q, const void* K, const void* V, const void* dO, const void* gdQ,
+                       const void* gdK, const void* gdV, const float* L, const float* D, const float* alpha,
+                       void* Qt, void* dOt, float* E, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, Qt, dOt, E});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_rows3, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, Qt, dOt, E,
               (hipStream_t)stream);
 }
 

@@ -30,7 +30,7 @@ def lib():
 def test_header_declares_the_entry_points():
     names = declared_functions()
     for n in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols",
-              "bob_supported", "bob_status_string", "bob_version"):
+              "attn_bob3_alpha_rows", "attn_bob3_rows", "bob_supported", "bob_status_string", "bob_version"):
         assert n in names
 
 
@@ -54,14 +54,16 @@ MISALIGNED = (1 << 20) + 8
 
 
 def call(lib, fn, dtype=fb.BOB_BF16, B=1, H=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None, causal=0):
-    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13}[fn]
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13,
+            "attn_bob3_alpha_rows": 6, "attn_bob3_rows": 13}[fn]
     ptrs = [ctypes.c_void_p(ptr) for _ in range(nptr)]
     if bad_index is not None:
         ptrs[bad_index] = ctypes.c_void_p(0)
     return getattr(lib, fn)(dtype, B, H, N, d, ctypes.c_float(scale), causal, *ptrs, None)
 
 
-FNS = ["attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols"]
+FNS = ["attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols", "attn_bob3_alpha_rows",
+       "attn_bob3_rows"]
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -85,7 +87,8 @@ def test_rejects_bad_arguments_without_launching(lib, fn):
 
 @pytest.mark.parametrize("fn", FNS)
 def test_every_pointer_is_checked(lib, fn):
-    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13}[fn]
+    nptr = {"attn_fwd_lse": 5, "attn_bwd": 10, "attn_bob_pass1_rows": 15, "attn_bob_pass2_cols": 13,
+            "attn_bob3_alpha_rows": 6, "attn_bob3_rows": 13}[fn]
     optional = {"attn_bob_pass1_rows": {10}}.get(fn, set())   # dQ may be NULL
     for i in range(nptr):
         if i not in optional:

@@ -189,6 +189,21 @@ def test_affine_fusion_matches_closed_form():
             assert diff <= 1e-12 * (1.0 + np.linalg.norm(c[key])), key
 
 
+def test_threepass_route_matches_closed_form():
+    """The three-pass control route (alpha first, then the delayed E
+    correction) reaches the closed form of eqs. 6-7, dense and causal."""
+    rng = np.random.default_rng(55)
+    for n, d in ((1, 3), (17, 8), (40, 16)):
+        for causal in (False, True):
+            args = rand_inputs(n, d, rng)
+            tau = 1 / np.sqrt(d)
+            a = bo.bob_threepass_head(*args, tau, causal)
+            c = bo.bob_head(*args, tau, causal)
+            for key in ("Qt", "dOt", "alpha", "E"):
+                diff = np.linalg.norm(a[key] - c[key])
+                assert diff <= 1e-12 * (1.0 + np.linalg.norm(c[key])), (key, causal)
+
+
 # ---------------------------------------------------------- symmetry
 
 
