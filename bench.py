@@ -51,6 +51,10 @@ PAPER_TABLE1_MS = {256: 0.94, 512: 1.29, 1024: 2.57, 2048: 7.53, 4096: 25.80, 81
                    16384: 365.73, 32768: 1449.06, 65536: 5843.14, 131072: 23528.87, 262144: 94853.72}
 
 
+# Table 11 of the paper: the same setup at N=4096, causal B=4 H=12, by head dim.
+PAPER_TABLE11_MS = {32: 14.214, 64: 25.676, 128: 81.694}
+
+
 def pair_count(N, causal):
     """(query, key) pairs that carry a nonzero P per head: N^2, or N(N+1)/2 causal."""
     return N * (N + 1) / 2.0 if causal else float(N) * N
@@ -423,10 +427,14 @@ def main():
     pn = peak_n_summary()
     if pn is not None:
         line["peak_n"] = pn
+    ref, src = None, None
     if w.causal and (w.B, w.H, w.d) == (4, 12, 64) and w.N in PAPER_TABLE1_MS:
-        ref = PAPER_TABLE1_MS[w.N]
+        ref, src = PAPER_TABLE1_MS[w.N], "Table 1: one A100 80GB, Triton, causal B=4 H=12 d=64 bf16"
+    elif w.causal and (w.B, w.H, w.N) == (4, 12, 4096) and w.d in PAPER_TABLE11_MS:
+        ref, src = PAPER_TABLE11_MS[w.d], f"Table 11: one A100 80GB, Triton, causal B=4 H=12 N=4096 d={w.d} bf16"
+    if ref is not None:
         line["paper_context"] = {
-            "source": "Table 1: one A100 80GB, Triton, causal B=4 H=12 d=64 bf16; scope of the timing unstated",
+            "source": src + "; scope of the timing unstated",
             "paper_ms": ref, "this_bob_ms": round(bob_med, 3), "this_step_ms": round(wall / args.steps * 1e3, 3),
             "bob_speedup": round(ref / bob_med, 2), "step_speedup": round(ref / (wall / args.steps * 1e3), 2)}
     if not args.no_cpu_baseline:

@@ -20,7 +20,8 @@
  *  B, H, N, d  batch, heads, sequence length and head dimension.  Matrices
  *          are contiguous row-major [B, H, N, d] in the tensor dtype; row
  *          vectors (L, D, alpha, E) are contiguous fp32 [B, H, N].
- *          Supported head dimensions: d = 64 and d = 128 (both dtypes).
+ *          Supported head dimensions: d = 32, 64, 128, 256 for bf16 and
+ *          d = 32, 64, 128 for fp32 (bob_supported() reports the set).
  *  scale   the softmax scale tau of eq. 1 (the paper uses 1/sqrt(d)); any
  *          finite value is accepted.  L is the natural-log normalizer
  *          L_i = log sum_{j valid} exp(S_ij) with S = tau Q K^T.

@@ -164,31 +164,62 @@ template <typename T, int D> struct Geo {
   static constexpr int kNB = D / 16;                             // 16-dim output blocks
   static constexpr int kBlocks = kBS * kCPR / 64;                // 1 KB blocks per tile
 
-  // physical slot of logical chunk c in row r
+  // physical slot of logical chunk c in row r (d = 64, 128; a d = 256 row
+  // uses the d = 128 order in each of its 256-byte halves), and its inverse
   static __device__ __forceinline__ int phys(int r, int c) {
     if constexpr (sizeof(T) == 4) {
-      return c ^ (r & 15);
+      return c ^ (r & (kCPR >= 16 ? 15 : kCPR - 1));
     } else if constexpr (D == 128) {
       return 4 * ((((r >> 1) & 3) + (c >> 1)) & 3) + 2 * (c & 1) + (((c >> 3) & 1) ^ (r & 1));
+    } else if constexpr (D == 256) {
+      return 16 * (c >> 4) +
+             (4 * ((((r >> 1) & 3) + ((c & 15) >> 1)) & 3) + 2 * (c & 1) + (((c >> 3) & 1) ^ (r & 1)));
     } else {
       static_assert(D == 64, "head dim");
       return 4 * ((((r >> 2) & 1) + (c >> 1)) & 1) + 2 * (c & 1) + (((c >> 2) & 1) ^ ((r >> 1) & 1));
     }
   }
-  // inverse: logical chunk stored at physical slot p of row r
   static __device__ __forceinline__ int logical(int r, int p) {
     if constexpr (sizeof(T) == 4) {
-      return p ^ (r & 15);
+      return p ^ (r & (kCPR >= 16 ? 15 : kCPR - 1));
     } else if constexpr (D == 128) {
       const int nb = (((p & 1) ^ (r & 1)) << 2) | (((p >> 2) - ((r >> 1) & 3)) & 3);
       return 2 * nb + ((p >> 1) & 1);
+    } else if constexpr (D == 256) {
+      const int q = p & 15;
+      const int nb = (((q & 1) ^ (r & 1)) << 2) | (((q >> 2) - ((r >> 1) & 3)) & 3);
+      return 16 * (p >> 4) + 2 * nb + ((q >> 1) & 1);
     } else {
       const int nb = (((p & 1) ^ ((r >> 1) & 1)) << 1) | ((p >> 2) ^ ((r >> 2) & 1));
       return 2 * nb + ((p >> 1) & 1);
     }
   }
+  // d = 32 bf16 rows are only 64 bytes, so no permutation inside a row can
+  // pair the slots of four consecutive rows: row pairs are interleaved at
+  // 16-byte granularity instead (row 2i and 2i+1 share a 128-byte block,
+  // chunk c of both side by side), and the chunk order rotates by two with
+  // bit 2 of the row so the transposed reads stay on distinct slots.
+  static constexpr bool kPairRows = sizeof(T) == 2 && D == 32;
+
   // element offset of logical chunk c of tile row r
-  static __device__ __forceinline__ int chunk_off(int r, int c) { return r * D + phys(r, c) * kEPC; }
+  static __device__ __forceinline__ int chunk_off(int r, int c) {
+    if constexpr (kPairRows)
+      return kEPC * (8 * (r >> 1) + 2 * ((c + 2 * ((r >> 2) & 1)) & 3) + (r & 1));
+    else
+      return r * D + phys(r, c) * kEPC;
+  }
+  // inverse of chunk_off for the HBM -> LDS copy: the (row, chunk) whose 16
+  // bytes belong at tile slot q
+  static __device__ __forceinline__ void slot_source(int q, int& r, int& c) {
+    if constexpr (kPairRows) {
+      const int w = q & 7;
+      r = 2 * (q >> 3) + (w & 1);
+      c = ((w >> 1) - 2 * ((r >> 2) & 1)) & 3;
+    } else {
+      r = q / kCPR;
+      c = logical(r, q % kCPR);
+    }
+  }
 
   // score A-operand: row r, the lane group's chunk of MFMA step kk
   static __device__ __forceinline__ u32x4 read_chunk(const T FB_LDS* X, int r, int kk) {
@@ -286,9 +317,8 @@ __device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_L
   constexpr int kBlockElems = 1024 / (int)sizeof(T);
   const int l = lane_id(), w = wave_id();
   auto one = [&](const T* base, int t, int b) {
-    const int q = b * 64 + l;
-    const int r = q / G::kCPR;
-    const int c = G::logical(r, q % G::kCPR);
+    int r, c;
+    G::slot_source(b * 64 + l, r, c);
     const int row = min(s0 + r, N - 1);
     __builtin_amdgcn_global_load_lds(
         (const __attribute__((address_space(1))) void*)(base + (int64_t)row * D + c * G::kEPC),

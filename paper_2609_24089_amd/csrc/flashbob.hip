@@ -17,6 +17,11 @@ struct Shape {
   int mr, nw, occ, st;
 };
 template <typename T, int D> struct Cfg;
+template <> struct Cfg<bf16, 32> {
+  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
+  static constexpr Shape kP1{2, 4, 2, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
+  static constexpr Shape kAlpha{2, 4, 2, 2};
+};
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{1, 8, 2, 2}, kRows{1, 8, 2, 2}, kCols{1, 8, 2, 2};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 3};
@@ -26,6 +31,16 @@ template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{1, 8, 2, 3}, kRows{1, 4, 2, 2}, kCols{1, 4, 2, 2};
   static constexpr Shape kP1{1, 8, 2, 3}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 3};
   static constexpr Shape kAlpha{2, 4, 2, 2};
+};
+template <> struct Cfg<bf16, 256> {
+  static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
+  static constexpr Shape kAlpha{1, 4, 2, 2};
+};
+template <> struct Cfg<float, 32> {
+  static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
+  static constexpr Shape kAlpha{1, 4, 1, 2};
 };
 template <> struct Cfg<float, 64> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
@@ -49,6 +64,14 @@ struct Problem {
   int32_t causal;
 };
 
+// (dtype, head dim) pairs built into the library: bf16 d = 32, 64, 128, 256;
+// fp32 d = 32, 64, 128 (fp32 d = 256 would need twice the registers of bf16).
+bool supported(int32_t dtype, int64_t d) {
+  if (dtype == BOB_BF16) return d == 32 || d == 64 || d == 128 || d == 256;
+  if (dtype == BOB_F32) return d == 32 || d == 64 || d == 128;
+  return false;
+}
+
 // Returns BOB_OK to proceed, or an error; sets *empty for B*H*N == 0.
 int32_t check_problem(const Problem& p, bool* empty) {
   *empty = false;
@@ -56,7 +79,7 @@ int32_t check_problem(const Problem& p, bool* empty) {
   if (p.B < 0 || p.H < 0 || p.N < 0 || p.d < 1) return BOB_EINVAL;
   if (!std::isfinite(p.scale)) return BOB_EINVAL;
   if (p.causal != 0 && p.causal != 1) return BOB_EINVAL;
-  if (p.d != 64 && p.d != 128) return BOB_EUNSUPPORTED;
+  if (!supported(p.dtype, p.d)) return BOB_EUNSUPPORTED;
   if (p.B == 0 || p.H == 0 || p.N == 0) {
     *empty = true;
     return BOB_OK;
@@ -186,8 +209,11 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
 // Dispatch on (dtype, d) to a templated launcher.
 #define FB_DISPATCH(p, FN, ...)                                                  \
   do {                                                                           \
+    if ((p).dtype == BOB_BF16 && (p).d == 32) return FN<fb::bf16, 32>(__VA_ARGS__);  \
     if ((p).dtype == BOB_BF16 && (p).d == 64) return FN<fb::bf16, 64>(__VA_ARGS__);  \
     if ((p).dtype == BOB_BF16 && (p).d == 128) return FN<fb::bf16, 128>(__VA_ARGS__); \
+    if ((p).dtype == BOB_BF16 && (p).d == 256) return FN<fb::bf16, 256>(__VA_ARGS__); \
+    if ((p).dtype == BOB_F32 && (p).d == 32) return FN<float, 32>(__VA_ARGS__);  \
     if ((p).dtype == BOB_F32 && (p).d == 64) return FN<float, 64>(__VA_ARGS__);  \
     if ((p).dtype == BOB_F32 && (p).d == 128) return FN<float, 128>(__VA_ARGS__); \
     return BOB_EUNSUPPORTED;                                                     \
@@ -281,14 +307,15 @@ int32_t attn_bob3_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d
 }
 
 int32_t bob_supported(int32_t dtype, int64_t d) {
-  return (dtype == BOB_F32 || dtype == BOB_BF16) && (d == 64 || d == 128) ? 1 : 0;
+  return fb::supported(dtype, d) ? 1 : 0;
 }
 
 const char* bob_status_string(int32_t status) {
   switch (status) {
     case BOB_OK: return "BOB_OK: success";
     case BOB_EINVAL: return "BOB_EINVAL: invalid argument (size, scale, dtype, or NULL/misaligned pointer)";
-    case BOB_EUNSUPPORTED: return "BOB_EUNSUPPORTED: (dtype, head dim) not built; supported d = 64, 128";
+    case BOB_EUNSUPPORTED:
+      return "BOB_EUNSUPPORTED: (dtype, head dim) not built; bf16 d = 32, 64, 128, 256; fp32 d = 32, 64, 128";
     case BOB_ELAUNCH: return "BOB_ELAUNCH: HIP kernel launch failed";
     default: return "unknown bob_status";
   }

@@ -40,8 +40,11 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_supported_and_strings(lib):
-    assert lib.bob_supported(fb.BOB_BF16, 64) == 1 and lib.bob_supported(fb.BOB_BF16, 128) == 1
-    assert lib.bob_supported(fb.BOB_F32, 64) == 1 and lib.bob_supported(fb.BOB_F32, 128) == 1
+    for d in (32, 64, 128, 256):
+        assert lib.bob_supported(fb.BOB_BF16, d) == 1, d
+    for d in (32, 64, 128):
+        assert lib.bob_supported(fb.BOB_F32, d) == 1, d
+    assert lib.bob_supported(fb.BOB_F32, 256) == 0
     assert lib.bob_supported(fb.BOB_BF16, 96) == 0 and lib.bob_supported(7, 64) == 0
     for rc in range(4):
         assert lib.bob_status_string(rc).decode().startswith("BOB_")
@@ -76,7 +79,8 @@ def test_rejects_bad_arguments_without_launching(lib, fn):
     assert call(lib, fn, scale=float("inf")) == fb.BOB_EINVAL
     assert call(lib, fn, dtype=5) == fb.BOB_EINVAL
     assert call(lib, fn, d=96) == fb.BOB_EUNSUPPORTED
-    assert call(lib, fn, d=32) == fb.BOB_EUNSUPPORTED
+    assert call(lib, fn, d=16) == fb.BOB_EUNSUPPORTED
+    assert call(lib, fn, dtype=fb.BOB_F32, d=256) == fb.BOB_EUNSUPPORTED
     assert call(lib, fn, ptr=MISALIGNED) == fb.BOB_EINVAL
     assert call(lib, fn, ptr=0) == fb.BOB_EINVAL
     assert call(lib, fn, N=(1 << 30) + 1) == fb.BOB_EINVAL

@@ -42,8 +42,9 @@ class Workload:
 
 # The five dense workloads: a tiny fp32 case, a small bf16 case, the N=16K
 # d=128 case, a long-context N=64K case and the N=256K maximum-length case.
-# Two causal workloads follow at the shape of the paper's own kernel timings
-# (causal, B=4, H=12, d=64; Table 1), for comparison with those figures.
+# Causal workloads follow at the shape of the paper's own kernel timings
+# (causal, B=4, H=12; Table 1 at d=64, the head-dim sweep of Table 11 at
+# N=4096), for comparison with those figures.
 WORKLOADS = {
     "tiny_f32_n256_d64": Workload("tiny_f32_n256_d64", 1, 1, 256, 64, "f32", 0),
     "bf16_b2h8_n4096_d64": Workload("bf16_b2h8_n4096_d64", 2, 8, 4096, 64, "bf16", 1),
@@ -55,6 +56,9 @@ WORKLOADS = {
     "causal_bf16_b4h12_n65536_d64": Workload("causal_bf16_b4h12_n65536_d64", 4, 12, 65536, 64, "bf16", 6,
                                              causal=True),
 }
+for _d, _seed in ((32, 8), (64, 9), (128, 10), (256, 11)):
+    _n = f"causal_bf16_b4h12_n4096_d{_d}"
+    WORKLOADS[_n] = Workload(_n, 4, 12, 4096, _d, "bf16", _seed, causal=True)
 
 
 def make_inputs(B, H, N, d, dtype="bf16", seed=0, qk_scale=1.0, device="cpu"):
