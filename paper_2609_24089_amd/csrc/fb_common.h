@@ -408,6 +408,56 @@ __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& is
     cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
 }
+// stream_loop for a kernel that transforms the streamed row scalars once per
+// tile before use.  One wave (`owner`) copies the scalars of tile t just
+// before the matrices of tile t-1 (issue_s, LS loads), so they have landed
+// whenever those matrices have; after its end-of-iteration wait the owner
+// runs prep(t+1) (reads the raw copy, writes the transformed values) ahead of
+// the barrier that already publishes the next tile, so every wave sees them
+// in iteration t+1.  issue_m(tile, matrix stage) issues LT loads per wave;
+// issue_s(tile, scalar stage) and prep(tile, scalar stage, transformed slot)
+// run on the owner only; body(tile, matrix stage, transformed slot).
+template <int NSTAGE, int LT, int LS, class IssueS, class IssueM, class Prep, class Body>
+__device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool owner, IssueS&& issue_s,
+                                               IssueM&& issue_m, Prep&& prep, Body&& body) {
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  const int n = it_end - it_begin;
+  if (owner && n > 0) issue_s(it_begin, 0);
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < n) {
+      if (owner && st + 1 < n) issue_s(it_begin + st + 1, st + 1);
+      issue_m(it_begin + st, st);
+    }
+  wait_vm<0>();
+  if (owner && n > 0) prep(it_begin, 0, 0);
+  __syncthreads();
+  int cur = 0;  // matrix stage of the current tile
+  for (int k = 0; k < n; ++k) {
+    const int nx = k + NSTAGE - 1;  // matrices fetched during this iteration
+    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+    if (nx < n) {
+      if (owner && nx + 1 < n) issue_s(it_begin + nx + 1, (nx + 1) % NSTAGE);
+      issue_m(it_begin + nx, nxs);
+    }
+    body(it_begin + k, cur, k & 1);
+    // the next tile's matrices (and, on the owner, the scalars of the tile
+    // after) must have landed; with three stages this iteration's copies may
+    // still be in flight
+    if (NSTAGE == 3 && nx < n) {
+      if (owner && nx + 1 < n)
+        wait_vm<LT + LS>();
+      else
+        wait_vm<LT>();
+    } else {
+      wait_vm<0>();
+    }
+    if (owner && k + 1 < n) prep(it_begin + k + 1, (k + 1) % NSTAGE, (k + 1) & 1);
+    __syncthreads();
+    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
+  }
+}
+
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile, copied HBM ->
 // LDS with global_load_lds_dword: one wave instruction moves two kBS-float
 // vectors (lanes 0..31 read `a`, lanes 32..63 read `b`) to dst[0 .. 63].

@@ -703,7 +703,9 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][3 * G::kTileElems];
-  __shared__ __attribute__((aligned(16))) float sc[NSTAGE][4 * kBS];
+  // raw L, D, alpha, E of NSTAGE tiles, and two slots of transformed ones
+  __shared__ __attribute__((aligned(16))) float rawsc[NSTAGE][4 * kBS];
+  __shared__ __attribute__((aligned(16))) float tsc[2][4 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -730,25 +732,27 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
   typename E::TFrag fPh[MC], fSt[MC], fdS[MC];
 
-  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
-  auto elementwise = [&](const float FB_LDS* Ls) {
+  // Transformed row scalars (tsc, per streamed row): T0 = -L log2e, T1 = -D,
+  // T2 = -alpha / tau, T3 = -(alpha D + E).  The score MFMAs start from
+  // T1, T2, T3, so they produce dd = dP - D, u = F / tau - alpha / tau and
+  // C - (alpha D + E) directly, and with h = tau u and
+  // Pt - E = tau u dd + C - (alpha D + E):
+  //   P h = tau (p u),  St = p (tau u dd + cc),  dS = p dd.
+  // The tau of P h is applied to Vt once, at the end.
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf).
+  auto elementwise = [&]() {
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
-      const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ls + kBS + 16 * sb + 4 * g);
-      const floatx4 av4 = *(const floatx4 FB_LDS*)(Ls + 2 * kBS + 16 * sb + 4 * g);
-      const floatx4 ev4 = *(const floatx4 FB_LDS*)(Ls + 3 * kBS + 16 * sb + 4 * g);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
           const float p = fast_exp2(s[sb][mc][r]);
-          const float fv = f[sb][mc][r] * scale;
-          const float dpv = dp[sb][mc][r];
-          const float dd = dpv - dv4[r];
-          const float pt = __builtin_fmaf(fv, dd, cc[sb][mc][r]) - av4[r] * dpv;
+          const float u = f[sb][mc][r];
+          const float dd = dp[sb][mc][r];
           const int i = 4 * sb + r;
-          fPh[mc].set(i, p * (fv - av4[r]));
-          fSt[mc].set(i, p * (pt - ev4[r]));
+          fPh[mc].set(i, p * u);
+          fSt[mc].set(i, p * __builtin_fmaf(scale, u * dd, cc[sb][mc][r]));
           fdS[mc].set(i, p * dd);
         }
       }
@@ -758,26 +762,49 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
-  stream_loop<NSTAGE, tile_loads<T, D, NW, 3>()>(
-      it_begin, nT,
-      [&](int it, int st) {
-        if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);
-        if (wave_id() == 1)
-          issue_scalar_pair((float FB_LDS*)sc[st] + 2 * kBS, alpha_in + soff, E_in + soff, it * kBS, N);
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N);
+  const float inv_scale = 1.0f / scale;
+  stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 3>(), 2>(
+      it_begin, nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      [&](int it, int rs) {
+        float FB_LDS* dst = (float FB_LDS*)rawsc[rs];
+        issue_scalar_pair(dst, L + soff, Dv + soff, it * kBS, N);
+        issue_scalar_pair(dst + 2 * kBS, alpha_in + soff, E_in + soff, it * kBS, N);
       },
-      [&](int it, int st) {
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int rs, int ts) {
+        (void)it;
+        if (l < kBS) {
+          const float FB_LDS* raw = (const float FB_LDS*)rawsc[rs];
+          float FB_LDS* t = (float FB_LDS*)tsc[ts];
+          const float Lr = raw[l], Dr = raw[kBS + l], ar = raw[2 * kBS + l], Er = raw[3 * kBS + l];
+          t[l] = -Lr * kLog2e;
+          t[kBS + l] = -Dr;
+          t[2 * kBS + l] = -ar * inv_scale;
+          t[3 * kBS + l] = -__builtin_fmaf(ar, Dr, Er);
+        }
+      },
+      [&](int it, int st, int ts) {
         const int s0 = it * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
         if (mode == 0) return;
         const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
         const T FB_LDS* UQs = Qs + G::kTileElems;
         const T FB_LDS* dOs = UQs + G::kTileElems;
-        // score tiles [s = query][t = key]
+        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ts];
+        // score tiles [s = query][t = key], started from the row terms
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 2; ++sb) {
+          const floatx4 t1 = *(const floatx4 FB_LDS*)(Ts + kBS + 16 * sb + 4 * g);
+          const floatx4 t2 = *(const floatx4 FB_LDS*)(Ts + 2 * kBS + 16 * sb + 4 * g);
+          const floatx4 t3 = *(const floatx4 FB_LDS*)(Ts + 3 * kBS + 16 * sb + 4 * g);
 #pragma unroll
-          for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = f[sb][mc] = cc[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+          for (int mc = 0; mc < MC; ++mc) {
+            s[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+            dp[sb][mc] = t1;
+            f[sb][mc] = t2;
+            cc[sb][mc] = t3;
+          }
+        }
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -789,23 +816,22 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
 #pragma unroll
             for (int mc = 0; mc < MC; ++mc) {
               s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
-              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP = dO V^T
-              f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // U_Q K^T
-              f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       // + Q U_K^T
-              cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C = dO U_V^T
+              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP - D
+              f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // (U_Q K^T
+              f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       //  + Q U_K^T) - alpha / tau
+              cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C - (alpha D + E)
             }
           }
-        const float FB_LDS* Ls = (const float FB_LDS*)sc[st];
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
-          const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+          const floatx4 t0 = *(const floatx4 FB_LDS*)(Ts + 16 * sb + 4 * g);
 #pragma unroll
           for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, -lv[r] * kLog2e);
+            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, t0[r]);
         }
         if (mode == 2) mask_tile<false>(s, s0, col0 + j, N, causal != 0);
-        elementwise(Ls);
+        elementwise();
 #pragma unroll
         for (int nb = 0; nb < G::kNB; ++nb) {
           const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
@@ -827,7 +853,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
       for (int nb = 0; nb < G::kNB; ++nb) {
         const int64_t off = hoff + (int64_t)col * D + 16 * nb + 4 * g;
         E::store4(Kt + off, aK[nb][mc] * scale);
-        E::store4(Vt + off, aV[nb][mc]);
+        E::store4(Vt + off, aV[nb][mc] * scale);
       }
     }
   }
