@@ -453,7 +453,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = f[sb][mb] = cc[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int mb = 0; mb < MR; ++mb) {
+        s[sb][mb] = f[sb][mb] = cc[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        dp[sb][mb] = floatx4{-drow[mb], -drow[mb], -drow[mb], -drow[mb]};  // the dP tile starts at -D
+      }
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -466,7 +469,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
 #pragma unroll
         for (int mb = 0; mb < MR; ++mb) {
           s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);        // S^T = K Q^T
-          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);     // dP^T = V dO^T
+          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);     // (dP - D)^T = V dO^T - D
           f[sb][mb] = E::mma_chunk(ak, uqf[mb][kk], f[sb][mb]);       // (U_Q K^T)^T
           f[sb][mb] = E::mma_chunk(auk, qf[mb][kk], f[sb][mb]);       // + (Q U_K^T)^T
           cc[sb][mb] = E::mma_chunk(auv, dof[mb][kk], cc[sb][mb]);    // C^T = U_V dO^T
@@ -483,12 +486,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         for (int r = 0; r < 4; ++r) {
           const float p = fast_exp2(s[sb][mb][r]);
           const float fv = f[sb][mb][r] * scale;
-          const float dpv = dp[sb][mb][r];
-          const float dd = dpv - drow[mb];
+          const float dd = dp[sb][mb][r];                         // dP - D
           const int i = 4 * sb + r;
           if constexpr (kThree) {
             // Pt with alpha known; fPF carries P h (h = F - alpha) here
-            const float pt = __builtin_fmaf(-arow[mb], dpv, __builtin_fmaf(fv, dd, cc[sb][mb][r]));
+            const float pt = __builtin_fmaf(-arow[mb], dd + drow[mb], __builtin_fmaf(fv, dd, cc[sb][mb][r]));
             const float ppt = p * pt;
             e0[mb] += ppt;
             fPF[mb].set(i, p * (fv - arow[mb]));
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           }
           fP[mb].set(i, p);
           fPdd[mb].set(i, p * dd);
-          if constexpr (kForm == kSixAcc) fPdp[mb].set(i, p * dpv);
+          if constexpr (kForm == kSixAcc) fPdp[mb].set(i, p * (dd + drow[mb]));
         }
     }
   };
