@@ -125,3 +125,27 @@ def test_deterministic_bitwise():
     b = run_gpu_path(x, 0.1)
     for k in OUTS:
         assert torch.equal(a[k], b[k]), k
+
+
+GRID_CASES = [
+    # B, H, N, d, dtype, seed, causal: many heads, workgroup counts that are
+    # and are not multiples of the 8 XCDs (the block remap has both paths)
+    (5, 13, 41, 64, "bf16", 140, False),
+    (8, 8, 200, 128, "bf16", 141, False),
+    (3, 7, 100, 128, "bf16", 142, True),
+    (16, 4, 64, 64, "f32", 143, True),
+]
+
+
+@pytest.mark.parametrize("case", GRID_CASES, ids=lambda c: f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{c[4]}{'c' if c[6] else ''}")
+def test_many_heads_grid_mapping(case):
+    B, H, N, d, dt, seed, causal = case
+    say(f"[grid] B{B} H{H} N{N} d{d} {dt} causal={causal}")
+    x = make_inputs(B, H, N, d, dt, seed)
+    scale = 1.0 / np.sqrt(d)
+    ref = oracle_full(x, scale, causal=causal)
+    out = run_gpu_path(to_dev(x), scale, causal=causal)
+    errs = {k: nrel(as_f64(out[k]), ref[k]) for k in ("O", "L", "dQ", "dK", "dV", "alpha", "E", "Qt", "dOt", "Kt", "Vt")}
+    say("   errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL[dt], (k, e)
