@@ -41,6 +41,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+// forward: growth of a row maximum (log2 units) that forces a rescale
+constexpr float kRescaleLog2 = 8.f;
 constexpr int kBS = 32;  // streamed rows per tile (two 16-row MFMA sub-blocks)
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }

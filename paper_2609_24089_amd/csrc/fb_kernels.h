@@ -65,19 +65,26 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
           mx = fmaxf(mx, s[sb][mb][r]);
         }
       mx = group_max(mx);
-      const float mnew = fmaxf(mrun[mb], mx);
-      const float corr = fast_exp2(mrun[mb] - mnew);
-      mrun[mb] = mnew;
-      float ls = lsum[mb] * corr;
+      // The reference maximum only moves when some row of the wave has grown
+      // by more than 2^8: the exponents stay <= 8, P <= 256, and the stale
+      // reference cancels in O = sum(P v) / sum(P) and in L = m + log2 sum(P).
+      // Most tiles then skip the rescale of the output accumulators.
+      if (__builtin_amdgcn_ballot_w64(mx > mrun[mb] + kRescaleLog2) != 0) {
+        const float mnew = fmaxf(mrun[mb], mx);
+        const float corr = fast_exp2(mrun[mb] - mnew);
+        mrun[mb] = mnew;
+        lsum[mb] *= corr;
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
+      }
+      float ls = lsum[mb];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float p = fast_exp2(x[i] - mnew);
+        const float p = fast_exp2(x[i] - mrun[mb]);
         ls += p;
         pf[mb].set(i, p);
       }
       lsum[mb] = ls;
-#pragma unroll
-      for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
     }
   };
 
