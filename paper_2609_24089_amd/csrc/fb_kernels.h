@@ -185,7 +185,8 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
   floatx4 s[2][MR], dp[2][MR];
   typename E::TFrag dsf[MR];
 
-  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf); dp holds
+  // dP - D (the MFMA started from -D)
   auto elementwise = [&]() {
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb)
@@ -194,7 +195,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float p = fast_exp2(s[sb][mb][r]);
-          dsf[mb].set(4 * sb + r, p * (dp[sb][mb][r] - drow[mb]));
+          dsf[mb].set(4 * sb + r, p * dp[sb][mb][r]);
         }
   };
 
@@ -213,7 +214,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-          for (int mb = 0; mb < MR; ++mb) s[sb][mb] = dp[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+          for (int mb = 0; mb < MR; ++mb) {
+            s[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            dp[sb][mb] = floatx4{-drow[mb], -drow[mb], -drow[mb], -drow[mb]};
+          }
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -265,7 +269,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
   __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
-  __shared__ __attribute__((aligned(16))) float sc[NSTAGE][2 * kBS];
+  // raw L, D of NSTAGE tiles, and two slots of transformed ones:
+  // T0 = -L log2e (the exponent offset), T1 = -D (the dP tile's start value)
+  __shared__ __attribute__((aligned(16))) float rawsc[NSTAGE][2 * kBS];
+  __shared__ __attribute__((aligned(16))) float tsc[2][2 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
@@ -289,42 +296,53 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   floatx4 s[2][MC], dp[2][MC];
   typename E::TFrag pf[MC], dsf[MC];
 
-  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
-  auto elementwise = [&](const float FB_LDS* Ls) {
-    const float FB_LDS* Ds = Ls + kBS;
+  // s holds exponents s*tau*log2e - L*log2e (masked entries -inf); dp holds
+  // dP - D (the MFMA started from -D)
+  auto elementwise = [&]() {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const floatx4 dv4 = *(const floatx4 FB_LDS*)(Ds + 16 * sb + 4 * g);
+    for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int mc = 0; mc < MC; ++mc) {
           const float p = fast_exp2(s[sb][mc][r]);
           pf[mc].set(4 * sb + r, p);
-          dsf[mc].set(4 * sb + r, p * (dp[sb][mc][r] - dv4[r]));
+          dsf[mc].set(4 * sb + r, p * dp[sb][mc][r]);
         }
-    }
   };
 
   const T* const src[2] = {Q + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
-  stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
-      it_begin, nT,
-      [&](int it, int st) {
-        if (wave_id() == 0) issue_scalar_pair((float FB_LDS*)sc[st], L + soff, Dv + soff, it * kBS, N);
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N);
+  stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 2>(), 1>(
+      it_begin, nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      [&](int it, int rs) { issue_scalar_pair((float FB_LDS*)rawsc[rs], L + soff, Dv + soff, it * kBS, N); },
+      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int rs, int ts) {
+        (void)it;
+        if (l < kBS) {
+          const float FB_LDS* raw = (const float FB_LDS*)rawsc[rs];
+          float FB_LDS* t = (float FB_LDS*)tsc[ts];
+          t[l] = -raw[l] * kLog2e;
+          t[kBS + l] = -raw[kBS + l];
+        }
       },
-      [&](int it, int st) {
+      [&](int it, int st, int ts) {
         const int s0 = it * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
         if (mode == 0) return;
         const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
         const T FB_LDS* dOs = Qs + G::kTileElems;
+        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ts];
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < 2; ++sb) {
+          const floatx4 t1 = *(const floatx4 FB_LDS*)(Ts + kBS + 16 * sb + 4 * g);
 #pragma unroll
-          for (int mc = 0; mc < MC; ++mc) s[sb][mc] = dp[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+          for (int mc = 0; mc < MC; ++mc) {
+            s[sb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+            dp[sb][mc] = t1;
+          }
+        }
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -338,17 +356,16 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
               dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
             }
           }
-        const float FB_LDS* Ls = (const float FB_LDS*)sc[st];
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
-          const floatx4 lv = *(const floatx4 FB_LDS*)(Ls + 16 * sb + 4 * g);
+          const floatx4 t0 = *(const floatx4 FB_LDS*)(Ts + 16 * sb + 4 * g);
 #pragma unroll
           for (int mc = 0; mc < MC; ++mc)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, -lv[r] * kLog2e);
+            for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, t0[r]);
         }
         if (mode == 2) mask_tile<false>(s, s0, col0 + j, N, causal != 0);
-        elementwise(Ls);
+        elementwise();
 #pragma unroll
         for (int nb = 0; nb < G::kNB; ++nb) {
           const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
