@@ -416,7 +416,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
 // ===========================================================================
 enum Pass1Form : int { kSixAcc = 0, kWithDQ = 1, kAlphaGiven = 2 };
 
-template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm, int DSPLIT>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
@@ -450,10 +450,17 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     drow[mb] = row < N ? Dv[soff + row] : 0.f;
     arow[mb] = (kThree && row < N) ? alpha_in[soff + row] : 0.f;
   }
-  constexpr int kNR = (kForm == kSixAcc) ? G::kNB : 1;  // R accumulator only in the six-accumulator form
-  floatx4 aDO[G::kNB][MR], aOM[G::kNB][MR], aB[G::kNB][MR], aR[kNR][MR];
+  // With DSPLIT = 2 the grid's second dimension picks which half of the head
+  // dims this workgroup accumulates and writes; both halves form the full
+  // score tiles (and the row scalars, written by half 0 only).
+  static_assert(G::kNB % DSPLIT == 0, "head-dim split");
+  constexpr int kNBh = G::kNB / DSPLIT;
+  const int nb0 = DSPLIT == 1 ? 0 : (int)blockIdx.y * kNBh;
+  const bool write_scalars = DSPLIT == 1 || blockIdx.y == 0;
+  constexpr int kNR = (kForm == kSixAcc) ? kNBh : 1;  // R accumulator only in the six-accumulator form
+  floatx4 aDO[kNBh][MR], aOM[kNBh][MR], aB[kNBh][MR], aR[kNR][MR];
 #pragma unroll
-  for (int nb = 0; nb < G::kNB; ++nb)
+  for (int nb = 0; nb < kNBh; ++nb)
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb) aDO[nb][mb] = aOM[nb][mb] = aB[nb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -540,11 +547,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T FB_LDS* UKs = Vs + G::kTileElems;
     const T FB_LDS* UVs = UKs + G::kTileElems;
 #pragma unroll
-    for (int nb = 0; nb < G::kNB; ++nb) {
-      const typename E::AFrag ak = G::load_afrag(Ks, 16 * nb);
-      const typename E::AFrag av = G::load_afrag(Vs, 16 * nb);
-      const typename E::AFrag auk = G::load_afrag(UKs, 16 * nb);
-      const typename E::AFrag auv = G::load_afrag(UVs, 16 * nb);
+    for (int nb = 0; nb < kNBh; ++nb) {
+      const typename E::AFrag ak = G::load_afrag(Ks, 16 * (nb0 + nb));
+      const typename E::AFrag av = G::load_afrag(Vs, 16 * (nb0 + nb));
+      const typename E::AFrag auk = G::load_afrag(UKs, 16 * (nb0 + nb));
+      const typename E::AFrag auv = G::load_afrag(UVs, 16 * (nb0 + nb));
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) {
         aB[nb][mb] = E::mma_acc(ak, fP[mb], aB[nb][mb]);
@@ -587,10 +594,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     if constexpr (kThree) {
       const float ee = group_sum(e0[mb]);
       if (row < N) {
-        if (g == 0) E_out[soff + row] = ee;
+        if (g == 0 && write_scalars) E_out[soff + row] = ee;
 #pragma unroll
-        for (int nb = 0; nb < G::kNB; ++nb) {
-          const int64_t off = hoff + (int64_t)row * D + 16 * nb + 4 * g;
+        for (int nb = 0; nb < kNBh; ++nb) {
+          const int64_t off = hoff + (int64_t)row * D + 16 * (nb0 + nb) + 4 * g;
           E::store4(dOt + off, aDO[nb][mb]);
           E::store4(Qt + off, scale * (aOM[nb][mb] - ee * aB[nb][mb]));
         }
@@ -601,13 +608,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const float e0s = group_sum(e0[mb]);
     const float ee = e0s - al * drow[mb];
     if (row < N) {
-      if (g == 0) {
+      if (g == 0 && write_scalars) {
         alpha_out[soff + row] = al;
         E_out[soff + row] = ee;
       }
 #pragma unroll
-      for (int nb = 0; nb < G::kNB; ++nb) {
-        const int64_t off = hoff + (int64_t)row * D + 16 * nb + 4 * g;
+      for (int nb = 0; nb < kNBh; ++nb) {
+        const int64_t off = hoff + (int64_t)row * D + 16 * (nb0 + nb) + 4 * g;
         const floatx4 o = E::load4(O + off);
         E::store4(dOt + off, aDO[nb][mb] - al * o);
         if (kDQ) {

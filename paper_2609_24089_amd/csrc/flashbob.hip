@@ -12,9 +12,10 @@ namespace {
 // Launch shapes per (element type, head dim) and kernel: MR = 16-row MFMA
 // blocks per wave, NW = waves per workgroup (a workgroup owns 16*MR*NW
 // stationary rows), OCC = waves per SIMD the register budget is held to, ST =
-// LDS pipeline stages (tiles in flight + 1).
+// LDS pipeline stages (tiles in flight + 1), DS = workgroups that share one
+// row block, each accumulating 1/DS of the head dims (Pass 1 only).
 struct Shape {
-  int mr, nw, occ, st;
+  int mr, nw, occ, st, ds = 1;
 };
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 32> {
@@ -34,7 +35,7 @@ template <> struct Cfg<bf16, 128> {
 };
 template <> struct Cfg<bf16, 256> {
   static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 4, 1, 2};
-  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
 };
 template <> struct Cfg<float, 32> {
@@ -149,7 +150,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   if (dQ != nullptr) {
     constexpr Shape c = Cfg<T, D>::kP1;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ>), dim3(g.total),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ, c.ds>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -157,7 +158,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc>), dim3(g.total),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc, c.ds>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -186,7 +187,7 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
   constexpr Shape c = Cfg<T, D>::kP1;
   const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven>), dim3(g.total),
+  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds>), dim3(g.total, c.ds),
                      dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)nullptr,
                      (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr, alpha,
                      (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
