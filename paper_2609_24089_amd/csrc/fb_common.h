@@ -413,12 +413,14 @@ __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& is
 // stream_loop for a kernel that transforms the streamed row scalars once per
 // tile before use.  One wave (`owner`) copies the scalars of tile t just
 // before the matrices of tile t-1 (issue_s, LS loads), so they have landed
-// whenever those matrices have; after its end-of-iteration wait the owner
-// runs prep(t+1) (reads the raw copy, writes the transformed values) ahead of
-// the barrier that already publishes the next tile, so every wave sees them
-// in iteration t+1.  issue_m(tile, matrix stage) issues LT loads per wave;
-// issue_s(tile, scalar stage) and prep(tile, scalar stage, transformed slot)
-// run on the owner only; body(tile, matrix stage, transformed slot).
+// by the time tile t-1 is consumed.  The body of tile t-1 calls prep_next()
+// exactly once on every path (after its score MFMAs are issued, so that the
+// owner's LDS round trip overlaps them): on the owner that runs prep(t), which
+// reads the raw copy and writes the transformed values into the slot that
+// tile t-2 used, and the barrier at the end of the iteration publishes them.
+// issue_m(tile, matrix stage) issues LT loads per wave; issue_s(tile, scalar
+// stage) and prep(tile, scalar stage, transformed slot) run on the owner only;
+// body(tile, matrix stage, transformed slot, prep_next).
 template <int NSTAGE, int LT, int LS, class IssueS, class IssueM, class Prep, class Body>
 __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool owner, IssueS&& issue_s,
                                                IssueM&& issue_m, Prep&& prep, Body&& body) {
@@ -442,7 +444,9 @@ __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool ow
       if (owner && nx + 1 < n) issue_s(it_begin + nx + 1, (nx + 1) % NSTAGE);
       issue_m(it_begin + nx, nxs);
     }
-    body(it_begin + k, cur, k & 1);
+    body(it_begin + k, cur, k & 1, [&]() {
+      if (owner && k + 1 < n) prep(it_begin + k + 1, (k + 1) % NSTAGE, (k + 1) & 1);
+    });
     // the next tile's matrices (and, on the owner, the scalars of the tile
     // after) must have landed; with three stages this iteration's copies may
     // still be in flight
@@ -454,7 +458,6 @@ __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool ow
     } else {
       wait_vm<0>();
     }
-    if (owner && k + 1 < n) prep(it_begin + k + 1, (k + 1) % NSTAGE, (k + 1) & 1);
     __syncthreads();
     cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }

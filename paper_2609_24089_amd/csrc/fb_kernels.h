@@ -327,10 +327,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
           t[kBS + l] = -raw[kBS + l];
         }
       },
-      [&](int it, int st, int ts) {
+      [&](int it, int st, int ts, auto&& prep_next) {
         const int s0 = it * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
-        if (mode == 0) return;
+        if (mode == 0) {
+          prep_next();
+          return;
+        }
         const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
         const T FB_LDS* dOs = Qs + G::kTileElems;
         const float FB_LDS* Ts = (const float FB_LDS*)tsc[ts];
@@ -376,6 +379,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
             dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
           }
         }
+        prep_next();
       });
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
@@ -816,10 +820,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
           t[3 * kBS + l] = -__builtin_fmaf(ar, Dr, Er);
         }
       },
-      [&](int it, int st, int ts) {
+      [&](int it, int st, int ts, auto&& prep_next) {
         const int s0 = it * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
-        if (mode == 0) return;
+        if (mode == 0) {
+          prep_next();
+          return;
+        }
         const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
         const T FB_LDS* UQs = Qs + G::kTileElems;
         const T FB_LDS* dOs = UQs + G::kTileElems;
@@ -855,6 +862,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
               cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C - (alpha D + E)
             }
           }
+        prep_next();
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
           const floatx4 t0 = *(const floatx4 FB_LDS*)(Ts + 16 * sb + 4 * g);
