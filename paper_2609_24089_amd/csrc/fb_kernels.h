@@ -18,7 +18,8 @@ namespace fb {
 // ===========================================================================
 // Forward: O = softmax(tau Q K^T + M) V and L = logsumexp(tau Q K^T + M)
 // (eq. 1 and the log-normalizer of Sec. 2).  Stationary: query rows.
-// Streamed: K, V.  Online softmax with a running row max.
+// Streamed: K, V.  Online softmax against a reference row maximum that
+// moves only when a row has grown past it by more than 2^8.
 // ===========================================================================
 template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
