@@ -22,6 +22,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import statistics
 import sys
 import time
@@ -60,11 +61,25 @@ def pair_count(N, causal):
     return N * (N + 1) / 2.0 if causal else float(N) * N
 
 
-def kernel_source_hash():
+def code_tokens(text):
+    """Kernel source text without comments and with whitespace collapsed, so
+    that the hash below changes with the code and not with its comments."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def kernel_source_hash(read=None):
+    """Hash of the kernel sources' code (see code_tokens); `read(name)` may
+    supply the text of each file instead of the working tree."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2609_24089_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        if read is None:
+            with open(os.path.join(ROOT, "paper_2609_24089_amd", "csrc", name)) as f:
+                text = f.read()
+        else:
+            text = read(name)
+        h.update(code_tokens(text).encode())
     return h.hexdigest()[:16]
 
 
