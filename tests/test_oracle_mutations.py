@@ -40,3 +40,21 @@ def test_fd_pin_catches_planted_mistake(name, monkeypatch):
     errs = [np.abs(out[key] - g).max() / max(1.0, np.abs(g).max())
             for key, g in zip(("Qt", "Kt", "Vt", "dOt"), fd)]
     assert max(errs) > 1e-4, (name, errs)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_torch_double_backward_pin_catches_planted_mistake(name, monkeypatch):
+    """The same planted mistakes also break agreement with torch's own double
+    backward (tests/test_oracle_autograd.py)."""
+    from tests.test_oracle_autograd import torch_bob
+    attr, wrong = MUTATIONS[name]
+    rng = np.random.default_rng(78)
+    n, d = 6, 4
+    args = rand_inputs(n, d, rng)
+    tau = 1 / np.sqrt(d)
+    _, ref = torch_bob(*args, tau, causal=False)   # computed before the mutation
+    monkeypatch.setattr(bo, attr, wrong)
+    out = bo.bob_head(*args, tau)
+    errs = [np.abs(out[key] - ref[key]).max() / max(1.0, np.abs(ref[key]).max())
+            for key in ("Qt", "Kt", "Vt", "dOt")]
+    assert max(errs) > 1e-4, (name, errs)
