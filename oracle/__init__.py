@@ -9,7 +9,8 @@ Every function takes plain NumPy arrays, works in float64 and materialises
 the full (or row-slab) N x N attention matrices, following the paper's
 definitions directly (Sec. 2 eqs. 1-3, Sec. 3.1 eqs. 4-5, Sec. 3.2 eqs. 6-8,
 App. A "Final assembled identities", App. B proof of Prop. 3.1, and the three-pass control schedule of App.
-"Three-pass versus two-pass").
+"Three-pass versus two-pass"), plus grouped key/value heads, the extension the
+paper names in its limitations.
 """
 from .bob_oracle import (  # noqa: F401
     forward_head,
@@ -27,4 +28,7 @@ from .bob_oracle import (  # noqa: F401
     bob_threepass,
     row_scalars,
     bob_cols,
+    bob_gqa,
+    expand_kv,
+    group_sum,
 )

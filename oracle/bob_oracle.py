@@ -310,6 +310,42 @@ def bob_affine(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
     return _batched(bob_affine_head, keys, Q, Q, K, V, dO, UQ, UK, UV, tau=tau, causal=causal)
 
 
+# --------------------------------------------------------------------------
+# Grouped-query attention (the extension named in the paper's limitations):
+# Hq query heads share Hkv key/value heads, G = Hq / Hkv, and query head h of a
+# batch attends with key/value head h // G.  The first-backward dK, dV of a
+# key/value head are the sums of its G query heads' contributions, so
+# <dK, U_K> + <dV, U_V> splits into one term per query head with the shared
+# U_K, U_V, and Phi (eq. 4) is the multi-head Phi with K, V, U_K, U_V repeated
+# per query head.  Hence Qt, dOt, alpha, E are the single-head definitions of
+# each query head, and Kt, Vt (like dK, dV) are summed over each group.
+# --------------------------------------------------------------------------
+
+
+def expand_kv(X, G):
+    """[B, Hkv, N, d] -> [B, Hkv * G, N, d]; query head h reads head h // G."""
+    return np.repeat(np.asarray(X, dtype=np.float64), G, axis=1)
+
+
+def group_sum(X, G):
+    """[B, Hkv * G, ...] -> [B, Hkv, ...]: sum over each group of G heads."""
+    X = np.asarray(X, dtype=np.float64)
+    return X.reshape((X.shape[0], X.shape[1] // G, G) + X.shape[2:]).sum(axis=2)
+
+
+def bob_gqa(Q, K, V, dO, UQ, UK, UV, tau, causal=False):
+    """BoB with grouped key/value heads: Q, dO, U_Q are [B, Hq, N, d] and
+    K, V, U_K, U_V are [B, Hkv, N, d] with Hq a multiple of Hkv.  Returns the
+    keys of `bob`, with Kt, Vt, dK, dV of shape [B, Hkv, N, d]."""
+    Hq, Hkv = Q.shape[1], K.shape[1]
+    assert Hkv >= 1 and Hq % Hkv == 0, (Hq, Hkv)
+    G = Hq // Hkv
+    out = bob(Q, expand_kv(K, G), expand_kv(V, G), dO, UQ, expand_kv(UK, G), expand_kv(UV, G), tau, causal=causal)
+    for key in ("Kt", "Vt", "dK", "dV"):
+        out[key] = group_sum(out[key], G)
+    return out
+
+
 def bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal=False):
     """Row-owned outputs of one head restricted to the query rows `rows`.
 
