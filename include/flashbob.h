@@ -107,6 +107,36 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
                             const float* L, const float* D, const float* alpha, const float* E,
                             void* Kt, void* Vt, void* stream);
 
+/* Grouped key/value heads (GQA; MQA when Hkv = 1), the extension the
+ * paper's limitations paragraph names and says the affine-fusion structure
+ * does not obstruct.  Hkv key/value heads are shared by the H query heads,
+ * H a multiple of Hkv: query head h of a batch entry uses key/value head
+ * h / (H / Hkv).  Query-side tensors (Q, dO, gdQ, O, dQ, Qt, dOt; L, D,
+ * alpha, E) are [B,H,N,d] or [B,H,N]; key-side tensors (K, V, gdK, gdV, dK,
+ * dV, Kt, Vt) are [B,Hkv,N,d].  The first-backward dK, dV of a key/value
+ * head sum its H / Hkv query heads' contributions, so Phi is the multi-head
+ * Phi with K, V, gdK, gdV repeated per query head: Qt, dOt, alpha, E are
+ * per query head and Kt, Vt sum over each group (written once, no atomics).
+ * Arguments and errors are those of the calls above, plus BOB_EINVAL when
+ * Hkv < 1 or H is not a multiple of Hkv for a non-empty problem.  With
+ * Hkv = H each call equals its multi-head counterpart. */
+int32_t attn_fwd_lse_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                         int32_t causal, const void* Q, const void* K, const void* V, void* O, float* L,
+                         void* stream);
+int32_t attn_bwd_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                     int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                     const float* L, void* dQ, void* dK, void* dV, float* D, void* stream);
+int32_t attn_bob_pass1_rows_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                const void* O, const void* dO, const void* gdQ, const void* gdK,
+                                const void* gdV, const float* L, const float* D, const void* dQ, void* Qt,
+                                void* dOt, float* alpha, float* E, void* stream);
+int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                const float* L, const float* D, const float* alpha, const float* E, void* Kt,
+                                void* Vt, void* stream);
+
 /* Three-pass control schedule (App. "Three-pass versus two-pass" and the
  * three-pass overlay of App. "Dependency graphs"): the schedule that the
  * affine fusion of Prop. 3.1 improves on, kept for the 2- vs 3-pass ablation

@@ -1,7 +1,8 @@
 """Exact attention backward-over-backward (FlashBoB) on MI355X.
 
-Thin Python binding over libflashbob.so (include/flashbob.h).  The four entry
-points keep the C names; each one only checks and marshals torch-ROCm tensors
+Thin Python binding over libflashbob.so (include/flashbob.h).  The entry
+points keep the C names (the grouped-query variants are chosen from the
+tensor shapes); each one only checks and marshals torch-ROCm tensors
 (device memory and the current stream) and calls the library, so every step
 of the computation runs in the gfx950 kernels.  There is no fallback: if the
 library is missing, importing the binding raises.
@@ -39,8 +40,14 @@ def load_library():
     lib.attn_bob_pass2_cols.argtypes = common + [vp] * 13 + [vp]
     lib.attn_bob3_alpha_rows.argtypes = common + [vp] * 6 + [vp]
     lib.attn_bob3_rows.argtypes = common + [vp] * 13 + [vp]
+    common_gqa = [i32, i64, i64, i64, i64, i64, f32, i32]  # ... H, Hkv, N, ...
+    lib.attn_fwd_lse_gqa.argtypes = common_gqa + [vp] * 5 + [vp]
+    lib.attn_bwd_gqa.argtypes = common_gqa + [vp] * 10 + [vp]
+    lib.attn_bob_pass1_rows_gqa.argtypes = common_gqa + [vp] * 15 + [vp]
+    lib.attn_bob_pass2_cols_gqa.argtypes = common_gqa + [vp] * 13 + [vp]
     for fn in ("attn_fwd_lse", "attn_bwd", "attn_bob_pass1_rows", "attn_bob_pass2_cols",
-               "attn_bob3_alpha_rows", "attn_bob3_rows"):
+               "attn_bob3_alpha_rows", "attn_bob3_rows", "attn_fwd_lse_gqa", "attn_bwd_gqa",
+               "attn_bob_pass1_rows_gqa", "attn_bob_pass2_cols_gqa"):
         getattr(lib, fn).restype = i32
     lib.bob_supported.argtypes = [i32, i64]
     lib.bob_supported.restype = i32
@@ -78,6 +85,24 @@ def _check_mats(*ts):
     return ref.shape
 
 
+def _check_groups(qside, kside):
+    """Query-side matrices [B, H, N, d] and key/value-side matrices
+    [B, Hkv, N, d] with H a multiple of Hkv (grouped-query attention; Hkv = H
+    is multi-head attention).  Returns (B, H, Hkv, N, d)."""
+    q, k = qside[0], kside[0]
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("matrices must be [B, H, N, d]")
+    B, H, N, d = q.shape
+    kB, Hkv, kN, kd = k.shape
+    if (kB, kN, kd) != (B, N, d) or k.dtype != q.dtype or k.device != q.device:
+        raise ValueError("key/value-side matrices must match the query side in B, N, d, dtype and device")
+    if (Hkv == 0 and H != 0) or (Hkv > 0 and H % Hkv != 0):
+        raise ValueError(f"the query heads ({H}) must be a multiple of the key/value heads ({Hkv})")
+    _check_mats(*qside)
+    _check_mats(*kside)
+    return B, H, Hkv, N, d
+
+
 def _check_rows(shape, *vs):
     for v in vs:
         if v.dtype != torch.float32 or tuple(v.shape) != tuple(shape[:3]) or not v.is_contiguous():
@@ -104,31 +129,39 @@ def _rows_empty(shape, like):
 
 
 def attn_fwd_lse(Q, K, V, scale, causal=False, out=None, stream=None):
-    """Forward attention (eq. 1): returns (O, L)."""
-    B, H, N, d = _check_mats(Q, K, V)
+    """Forward attention (eq. 1): returns (O, L).  K, V may have fewer heads
+    than Q (grouped-query attention, see include/flashbob.h)."""
+    B, H, Hkv, N, d = _check_groups((Q,), (K, V))
     if out is None:
         out = (torch.empty_like(Q), _rows_empty(Q.shape, Q))
     O, L = out
     _check_mats(Q, O)
     _check_rows(Q.shape, L)
     lib = load_library()
-    _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
-          _p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
+    if Hkv == H:
+        _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+    else:
+        _call(lib.attn_fwd_lse_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
     return O, L
 
 
 def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
-    """First backward (eqs. 2-3): returns (dQ, dK, dV, D)."""
-    B, H, N, d = _check_mats(Q, K, V, O, dO)
+    """First backward (eqs. 2-3): returns (dQ, dK, dV, D); dK, dV have K's shape."""
+    B, H, Hkv, N, d = _check_groups((Q, O, dO), (K, V))
     _check_rows(Q.shape, L)
     if out is None:
-        out = (torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(Q), _rows_empty(Q.shape, Q))
+        out = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(K), _rows_empty(Q.shape, Q))
     dQ, dK, dV, D = out
-    _check_mats(Q, dQ, dK, dV)
+    _check_mats(Q, dQ)
+    _check_mats(K, dK, dV)
     _check_rows(Q.shape, D)
     lib = load_library()
-    _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
-          _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
+    if Hkv == H:
+        _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+    else:
+        _call(lib.attn_bwd_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
     return dQ, dK, dV, D
 
 
@@ -138,7 +171,7 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal=False
 
     dQ (the first-backward output) is optional; when given, the kernel uses
     it in place of the R accumulator (see include/flashbob.h)."""
-    B, H, N, d = _check_mats(Q, K, V, O, dO, gdQ, gdK, gdV)
+    B, H, Hkv, N, d = _check_groups((Q, O, dO, gdQ), (K, V, gdK, gdV))
     if dQ is not None:
         _check_mats(Q, dQ)
     _check_rows(Q.shape, L, D)
@@ -148,24 +181,32 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal=False
     _check_mats(Q, Qt, dOt)
     _check_rows(Q.shape, alpha, E)
     lib = load_library()
-    _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
-          _p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
-          None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
+            None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
+    if Hkv == H:
+        _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+    else:
+        _call(lib.attn_bob_pass1_rows_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
+              *ptrs)
     return Qt, dOt, alpha, E
 
 
 def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal=False, out=None, stream=None):
-    """BoB Pass 2 (column-major): returns (Kt, Vt)."""
-    B, H, N, d = _check_mats(Q, K, V, dO, gdQ, gdK, gdV)
+    """BoB Pass 2 (column-major): returns (Kt, Vt), with K's shape."""
+    B, H, Hkv, N, d = _check_groups((Q, dO, gdQ), (K, V, gdK, gdV))
     _check_rows(Q.shape, L, D, alpha, E)
     if out is None:
-        out = (torch.empty_like(Q), torch.empty_like(Q))
+        out = (torch.empty_like(K), torch.empty_like(K))
     Kt, Vt = out
-    _check_mats(Q, Kt, Vt)
+    _check_mats(K, Kt, Vt)
     lib = load_library()
-    _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
-          _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
-          _p(Kt), _p(Vt), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
+            _p(Kt), _p(Vt), _stream(stream))
+    if Hkv == H:
+        _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+    else:
+        _call(lib.attn_bob_pass2_cols_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
+              *ptrs)
     return Kt, Vt
 
 

@@ -20,7 +20,9 @@ first-backward node reports no gradient for its O and L inputs.  dOt flows
 into whatever produced dO, which carries the loss curvature in O.
 
 Every step runs in the HIP kernels of libflashbob.so; the tensors must be
-contiguous [B, H, N, d] bf16 or fp32 on the ROCm device.
+contiguous [B, H, N, d] bf16 or fp32 on the ROCm device.  k and v may have
+fewer heads than q (grouped-query attention: query head h uses key/value
+head h // (H / Hkv)); their gradients then sum over each group.
 """
 import torch
 
@@ -53,7 +55,7 @@ class _AttentionBackwardFn(torch.autograd.Function):
     @staticmethod
     def backward(ctx, gdq, gdk, gdv):
         q, k, v, O, L, dO, D, dq = ctx.saved_tensors
-        cot = [torch.zeros_like(q) if g is None else g.contiguous() for g in (gdq, gdk, gdv)]
+        cot = [torch.zeros_like(x) if g is None else g.contiguous() for g, x in ((gdq, q), (gdk, k), (gdv, v))]
         Qt, dOt, alpha, E = attn_bob_pass1_rows(q, k, v, O, dO, *cot, L, D, ctx.scale, causal=ctx.causal, dQ=dq)
         Kt, Vt = attn_bob_pass2_cols(q, k, v, dO, *cot, L, D, alpha, E, ctx.scale, causal=ctx.causal)
         return Qt, Kt, Vt, None, None, dOt, None, None

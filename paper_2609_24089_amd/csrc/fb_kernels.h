@@ -10,6 +10,16 @@
 // with it the mask M_mask of eq. 1 is -inf where key > query, masked entries
 // get P = 0, tiles above the diagonal are skipped and diagonal tiles are
 // masked per element.  Rows past N are masked the same way.
+//
+// Every kernel also takes `grp`, the number of query heads that share one
+// key/value head (grouped-query attention, the extension the paper names in
+// its limitations; grp = 1 is multi-head attention).  Query-side tensors
+// (Q, dO, U_Q, O, dQ, Qt, dOt and the row scalars) have B*H heads and
+// key-side tensors (K, V, U_K, U_V, dK, dV, Kt, Vt) B*H/grp; query head bh
+// reads key/value head bh / grp.  Row kernels run one workgroup per query
+// head row block; column kernels one per key/value head column block, and
+// stream the grp query heads of that key/value head one after another, so
+// their key-side outputs sum over the group with no atomics.
 #pragma once
 #include "fb_common.h"
 
@@ -24,7 +34,7 @@ namespace fb {
 template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
-    T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale, int causal) {
+    T* __restrict__ O, float* __restrict__ L, int N, int nRB, int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
@@ -33,6 +43,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
   int bh, rb;
   map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t kvoff = (int64_t)(bh / grp) * N * D;  // key/value head of this query head
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int row0 = rb * BR + wave_id() * 16 * MR;
 
@@ -89,7 +100,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
     }
   };
 
-  const T* const src[2] = {K + hoff, V + hoff};
+  const T* const src[2] = {K + kvoff, V + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
@@ -148,7 +159,7 @@ template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const float* __restrict__ L,
-    T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale, int causal) {
+    T* __restrict__ dQ, float* __restrict__ Dout, int N, int nRB, int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
@@ -157,6 +168,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
   int bh, rb;
   map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
+  const int64_t kvoff = (int64_t)(bh / grp) * N * D;  // key/value head of this query head
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int row0 = rb * BR + wave_id() * 16 * MR;
 
@@ -200,7 +212,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
         }
   };
 
-  const T* const src[2] = {K + hoff, V + hoff};
+  const T* const src[2] = {K + kvoff, V + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
@@ -261,11 +273,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // First backward, column side: dV = P^T dO and dK = tau dS^T Q (eqs. 2-3).
 // Stationary: K, V rows.  Streamed: Q, dO tiles with their L and D.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA>
 __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
-    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal) {
+    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
@@ -278,7 +290,6 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
   int bh, rb;
   map_block(nRB, total, bh, rb);
   const int64_t hoff = (int64_t)bh * N * D;
-  const int64_t soff = (int64_t)bh * N;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int col0 = rb * BC + wave_id() * 16 * MC;
 
@@ -312,13 +323,26 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
         }
   };
 
-  const T* const src[2] = {Q + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
+  // With kGQA the streamed side runs over the grp query heads that share
+  // this key/value head, one after another: iteration it is tile
+  // it_begin + it % nTh of query head bh * grp + it / nTh.  Without it the
+  // streamed rows are those of head bh.
+  const int nTh = nT - it_begin;
+  auto qhead = [&](int it) { return kGQA ? bh * grp + it / nTh : bh; };
+  auto tile = [&](int it) { return kGQA ? it_begin + it % nTh : it; };
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 2>(), 1>(
-      it_begin, nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
-      [&](int it, int rs) { issue_scalar_pair((float FB_LDS*)rawsc[rs], L + soff, Dv + soff, it * kBS, N); },
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      kGQA ? 0 : it_begin, kGQA ? grp * nTh : nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      [&](int it, int rs) {
+        const int64_t qs = (int64_t)qhead(it) * N;
+        issue_scalar_pair((float FB_LDS*)rawsc[rs], L + qs, Dv + qs, tile(it) * kBS, N);
+      },
+      [&](int it, int st) {
+        const int64_t qo = (int64_t)qhead(it) * N * D;
+        const T* const src[2] = {Q + qo, dO + qo};
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], tile(it) * kBS, N);
+      },
       [&](int it, int rs, int ts) {
         (void)it;
         if (l < kBS) {
@@ -329,7 +353,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
         }
       },
       [&](int it, int st, int ts, auto&& prep_next) {
-        const int s0 = it * kBS;
+        const int s0 = tile(it) * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
         if (mode == 0) {
           prep_next();
@@ -428,7 +452,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ UK, const T* __restrict__ UV, const float* __restrict__ L,
     const float* __restrict__ Dv, const T* __restrict__ dQ, const float* __restrict__ alpha_in,
     T* __restrict__ Qt, T* __restrict__ dOt, float* __restrict__ alpha_out, float* __restrict__ E_out,
-    int N, int nRB, int total, float scale, int causal) {
+    int N, int nRB, int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr bool kDQ = kForm == kWithDQ;
@@ -440,6 +464,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
   const int64_t soff = (int64_t)bh * N;
+  const int64_t kvoff = (int64_t)(bh / grp) * N * D;  // key/value head of this query head
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int row0 = rb * BR + wave_id() * 16 * MR;
 
@@ -569,7 +594,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     }
   };
 
-  const T* const src[4] = {K + hoff, V + hoff, UK + hoff, UV + hoff};
+  const T* const src[4] = {K + kvoff, V + kvoff, UK + kvoff, UV + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
   stream_loop<NSTAGE, tile_loads<T, D, NW, 4>()>(
@@ -644,7 +669,7 @@ template <typename T, int D, int MR, int NW, int OCC, int NSTAGE>
 __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ UQ,
     const T* __restrict__ UK, const float* __restrict__ L, float* __restrict__ alpha_out, int N, int nRB,
-    int total, float scale, int causal) {
+    int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BR = 16 * MR * NW;
@@ -654,6 +679,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
   map_block(nRB, total, bh, rb, causal != 0);
   const int64_t hoff = (int64_t)bh * N * D;
   const int64_t soff = (int64_t)bh * N;
+  const int64_t kvoff = (int64_t)(bh / grp) * N * D;  // key/value head of this query head
   const int l = lane_id(), g = l >> 4, j = l & 15;
   (void)l;
   const int row0 = rb * BR + wave_id() * 16 * MR;
@@ -671,7 +697,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
   const float c = scale * kLog2e;
   floatx4 s[2][MR], f[2][MR];
 
-  const T* const src[2] = {K + hoff, UK + hoff};
+  const T* const src[2] = {K + kvoff, UK + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
@@ -730,13 +756,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 //   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
 // Writes Kt, Vt once; no atomics.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
     const float* __restrict__ alpha_in, const float* __restrict__ E_in,
-    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal) {
+    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp) {
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
@@ -748,7 +774,6 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   int bh, rb;
   map_block(nRB, total, bh, rb);
   const int64_t hoff = (int64_t)bh * N * D;
-  const int64_t soff = (int64_t)bh * N;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int col0 = rb * BC + wave_id() * 16 * MC;
 
@@ -797,18 +822,29 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
     }
   };
 
-  const T* const src[3] = {Q + hoff, UQ + hoff, dO + hoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
   const float inv_scale = 1.0f / scale;
+  // With kGQA the streamed side runs over the grp query heads that share
+  // this key/value head, one after another: iteration it is tile
+  // it_begin + it % nTh of query head bh * grp + it / nTh.  Without it the
+  // streamed rows are those of head bh.
+  const int nTh = nT - it_begin;
+  auto qhead = [&](int it) { return kGQA ? bh * grp + it / nTh : bh; };
+  auto tile = [&](int it) { return kGQA ? it_begin + it % nTh : it; };
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 3>(), 2>(
-      it_begin, nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      kGQA ? 0 : it_begin, kGQA ? grp * nTh : nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
       [&](int it, int rs) {
+        const int64_t qs = (int64_t)qhead(it) * N;
         float FB_LDS* dst = (float FB_LDS*)rawsc[rs];
-        issue_scalar_pair(dst, L + soff, Dv + soff, it * kBS, N);
-        issue_scalar_pair(dst + 2 * kBS, alpha_in + soff, E_in + soff, it * kBS, N);
+        issue_scalar_pair(dst, L + qs, Dv + qs, tile(it) * kBS, N);
+        issue_scalar_pair(dst + 2 * kBS, alpha_in + qs, E_in + qs, tile(it) * kBS, N);
       },
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) {
+        const int64_t qo = (int64_t)qhead(it) * N * D;
+        const T* const src[3] = {Q + qo, UQ + qo, dO + qo};
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], tile(it) * kBS, N);
+      },
       [&](int it, int rs, int ts) {
         (void)it;
         if (l < kBS) {
@@ -822,7 +858,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
         }
       },
       [&](int it, int st, int ts, auto&& prep_next) {
-        const int s0 = it * kBS;
+        const int s0 = tile(it) * kBS;
         const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
         if (mode == 0) {
           prep_next();

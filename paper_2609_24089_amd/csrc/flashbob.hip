@@ -58,12 +58,16 @@ constexpr int64_t kMaxN = int64_t(1) << 30;
 
 bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// H query heads per batch entry; Hkv key/value heads (H for multi-head
+// attention, a divisor of H for grouped-query attention).
 struct Problem {
   int32_t dtype;
   int64_t B, H, N, d;
   float scale;
   int32_t causal;
+  int64_t Hkv;
 };
+int group(const Problem& p) { return (int)(p.H / p.Hkv); }
 
 // (dtype, head dim) pairs built into the library: bf16 d = 32, 64, 128, 256;
 // fp32 d = 32, 64, 128 (fp32 d = 256 would need twice the registers of bf16).
@@ -80,6 +84,7 @@ int32_t check_problem(const Problem& p, bool* empty) {
   if (p.B < 0 || p.H < 0 || p.N < 0 || p.d < 1) return BOB_EINVAL;
   if (!std::isfinite(p.scale)) return BOB_EINVAL;
   if (p.causal != 0 && p.causal != 1) return BOB_EINVAL;
+  if (p.Hkv < 0 || (p.H > 0 && (p.Hkv < 1 || p.H % p.Hkv != 0))) return BOB_EINVAL;
   if (!supported(p.dtype, p.d)) return BOB_EUNSUPPORTED;
   if (p.B == 0 || p.H == 0 || p.N == 0) {
     *empty = true;
@@ -104,10 +109,11 @@ int32_t finish_launch() { return hipGetLastError() == hipSuccess ? BOB_OK : BOB_
 struct Grid {
   int nRB, total;
 };
-Grid grid_for(const Problem& p, int rows_per_block) {
+// Row kernels run over the query heads, column kernels over the key/value heads.
+Grid grid_for(const Problem& p, int rows_per_block, bool kv_heads = false) {
   Grid g;
   g.nRB = (int)((p.N + rows_per_block - 1) / rows_per_block);
-  g.total = (int)(p.B * p.H * g.nRB);
+  g.total = (int)(p.B * (kv_heads ? p.Hkv : p.H) * g.nRB);
   return g;
 }
 
@@ -118,7 +124,7 @@ int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V
   const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_fwd_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale, p.causal);
+                     (const T*)Q, (const T*)K, (const T*)V, (T*)O, L, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
   return finish_launch();
 }
 
@@ -131,13 +137,18 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, cr.mr, cr.nw, cr.occ, cr.st>), dim3(gr.total), dim3(64 * cr.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)O, (const T*)dO, L, (T*)dQ, Dv,
-                     (int)p.N, gr.nRB, gr.total, p.scale, p.causal);
+                     (int)p.N, gr.nRB, gr.total, p.scale, p.causal, group(p));
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
-  const Grid gc = grid_for(p, 16 * cc.mr * cc.nw);
-  hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
+  const Grid gc = grid_for(p, 16 * cc.mr * cc.nw, true);
+  if (group(p) == 1)
+    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, false>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
-                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal);
+                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal, group(p));
+  else
+    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
+                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal, group(p));
   return finish_launch();
 }
 
@@ -154,7 +165,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
-                       p.causal);
+                       p.causal, group(p));
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
@@ -162,7 +173,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
-                       p.causal);
+                       p.causal, group(p));
   }
   return finish_launch();
 }
@@ -176,7 +187,7 @@ int32_t launch_alpha3(const Problem& p, const void* Q, const void* K, const void
   (void)hipGetLastError();
   hipLaunchKernelGGL((bob3_alpha_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)UQ, (const T*)UK, L, alpha, (int)p.N, g.nRB, g.total,
-                     p.scale, p.causal);
+                     p.scale, p.causal, group(p));
   return finish_launch();
 }
 
@@ -190,7 +201,7 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
   hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds>), dim3(g.total, c.ds),
                      dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)nullptr,
                      (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr, alpha,
-                     (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal);
+                     (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
   return finish_launch();
 }
 
@@ -199,11 +210,16 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
                      const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
                      const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s) {
   constexpr Shape c = Cfg<T, D>::kP2;
-  const Grid g = grid_for(p, 16 * c.mr * c.nw);
+  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st>), dim3(g.total), dim3(64 * c.nw), 0, s,
+  if (group(p) == 1)
+    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, false>), dim3(g.total), dim3(64 * c.nw), 0, s,
                      (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
-                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal);
+                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
+  else
+    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, true>), dim3(g.total), dim3(64 * c.nw), 0, s,
+                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
+                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
   return finish_launch();
 }
 
@@ -229,7 +245,7 @@ extern "C" {
 
 int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                      const void* Q, const void* K, const void* V, void* O, float* L, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -241,7 +257,7 @@ int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, 
 int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                  const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -255,7 +271,7 @@ int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
                             const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                             const float* L, const float* D, const void* dQ, void* Qt, void* dOt,
                             float* alpha, float* E, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -271,7 +287,64 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
                             const void* gdQ, const void* gdK, const void* gdV, const float* L,
                             const float* D, const float* alpha, const float* E, void* Kt, void* Vt,
                             void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
+              (hipStream_t)stream);
+}
+
+// Grouped key/value heads: as above with Hkv key/value heads shared by the H
+// query heads (H a multiple of Hkv).
+int32_t attn_fwd_lse_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                         int32_t causal, const void* Q, const void* K, const void* V, void* O, float* L,
+                         void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, L});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_fwd, p, Q, K, V, O, L, (hipStream_t)stream);
+}
+
+int32_t attn_bwd_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                     int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                     const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
+  if (rc != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream);
+}
+
+int32_t attn_bob_pass1_rows_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                const void* O, const void* dO, const void* gdQ, const void* gdK,
+                                const void* gdV, const float* L, const float* D, const void* dQ, void* Qt,
+                                void* dOt, float* alpha, float* E, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, dO, gdQ, gdK, gdV, L, D, Qt, dOt, alpha, E});
+  if (rc != BOB_OK) return rc;
+  if (dQ != nullptr && !fb::aligned16(dQ)) return BOB_EINVAL;
+  FB_DISPATCH(p, fb::launch_pass1, p, Q, K, V, O, dO, gdQ, gdK, gdV, L, D, dQ, Qt, dOt, alpha, E,
+              (hipStream_t)stream);
+}
+
+int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                const float* L, const float* D, const float* alpha, const float* E, void* Kt,
+                                void* Vt, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -284,7 +357,7 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
 int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
                              int32_t causal, const void* Q, const void* K, const void* gdQ, const void* gdK,
                              const float* L, float* alpha, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;
@@ -297,7 +370,7 @@ int32_t attn_bob3_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d
                        const void* Q, const void* K, const void* V, const void* dO, const void* gdQ,
                        const void* gdK, const void* gdV, const float* L, const float* D, const float* alpha,
                        void* Qt, void* dOt, float* E, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal};
+  const Problem p{dtype, B, H, N, d, scale, causal, H};
   bool empty;
   int32_t rc = fb::check_problem(p, &empty);
   if (rc != BOB_OK || empty) return rc;

@@ -134,3 +134,54 @@ def test_attention_wrapper_rejects_host_tensors():
     x = torch.zeros(1, 1, 8, 64)
     with pytest.raises(ValueError, match="ROCm device"):
         fb.attention(x, x, x)
+
+
+GQA_NPTR = {"attn_fwd_lse_gqa": 5, "attn_bwd_gqa": 10, "attn_bob_pass1_rows_gqa": 15, "attn_bob_pass2_cols_gqa": 13}
+
+
+def call_gqa(lib, fn, H=4, Hkv=2, dtype=fb.BOB_BF16, B=1, N=16, d=64, scale=0.125, ptr=ALIGNED, bad_index=None,
+             causal=0):
+    ptrs = [ctypes.c_void_p(ptr) for _ in range(GQA_NPTR[fn])]
+    if bad_index is not None:
+        ptrs[bad_index] = ctypes.c_void_p(0)
+    return getattr(lib, fn)(dtype, B, H, Hkv, N, d, ctypes.c_float(scale), causal, *ptrs, None)
+
+
+def test_header_declares_the_grouped_entry_points():
+    names = declared_functions()
+    for n in GQA_NPTR:
+        assert n in names
+
+
+@pytest.mark.parametrize("fn", sorted(GQA_NPTR))
+def test_grouped_heads_are_validated(lib, fn):
+    assert call_gqa(lib, fn, H=4, Hkv=0) == fb.BOB_EINVAL
+    assert call_gqa(lib, fn, H=4, Hkv=-1) == fb.BOB_EINVAL
+    assert call_gqa(lib, fn, H=4, Hkv=3) == fb.BOB_EINVAL       # 4 is not a multiple of 3
+    assert call_gqa(lib, fn, H=4, Hkv=8) == fb.BOB_EINVAL       # more key/value heads than query heads
+    assert call_gqa(lib, fn, d=96) == fb.BOB_EUNSUPPORTED
+    assert call_gqa(lib, fn, scale=float("nan")) == fb.BOB_EINVAL
+    assert call_gqa(lib, fn, causal=2) == fb.BOB_EINVAL
+    assert call_gqa(lib, fn, ptr=MISALIGNED) == fb.BOB_EINVAL
+    # empty problems touch no memory
+    assert call_gqa(lib, fn, N=0, ptr=0) == fb.BOB_OK
+    assert call_gqa(lib, fn, H=0, Hkv=0, ptr=0) == fb.BOB_OK
+
+
+@pytest.mark.parametrize("fn", sorted(GQA_NPTR))
+def test_grouped_entry_points_check_every_pointer(lib, fn):
+    optional = {"attn_bob_pass1_rows_gqa": {10}}.get(fn, set())   # dQ may be NULL
+    for i in range(GQA_NPTR[fn]):
+        if i not in optional:
+            assert call_gqa(lib, fn, bad_index=i) == fb.BOB_EINVAL, i
+
+
+def test_binding_checks_group_shapes():
+    import torch
+    q = torch.zeros(1, 4, 8, 64, dtype=torch.bfloat16)
+    k3 = torch.zeros(1, 3, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="multiple of the key/value heads"):
+        fb.attn_fwd_lse(q, k3, k3, 0.125)
+    k2 = torch.zeros(1, 2, 9, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="must match the query side"):
+        fb.attn_fwd_lse(q, k2, k2, 0.125)

@@ -75,6 +75,20 @@ def make_inputs(B, H, N, d, dtype="bf16", seed=0, qk_scale=1.0, device="cpu"):
     return out
 
 
+def make_gqa_inputs(B, H, Hkv, N, d, dtype="bf16", seed=0, device="cpu"):
+    """Grouped-query inputs: Q, dO, UQ with H heads and K, V, UK, UV with Hkv
+    heads, drawn in the order of NAMES from one seeded generator as in
+    make_inputs (N(0,1) float32, then cast)."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(int(seed))
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    out = {}
+    for name in NAMES:
+        heads = Hkv if name in ("K", "V", "UK", "UV") else H
+        out[name] = torch.randn((B, heads, N, d), generator=gen, dtype=torch.float32).to(tdt).to(device)
+    return out
+
+
 def workload_inputs(w: Workload, device="cpu"):
     return make_inputs(w.B, w.H, w.N, w.d, w.dtype, w.seed, w.qk_scale, device)
 
