@@ -171,6 +171,20 @@ const char* bob_status_string(int32_t status);
 /* Static version string of the library. */
 const char* bob_version(void);
 
+/* How the column-owned kernels (the dK, dV half of attn_bwd, and Pass 2)
+ * spread a key/value column block over a CU.  By default (mode 0) a column
+ * block whose grid has no more workgroups than the device has compute units
+ * (few key/value heads and short sequences, e.g. multi-query attention) is
+ * given two wave sets in one workgroup, which take alternate streamed tiles
+ * and add their fp32 partial sums in a fixed order at the end; larger grids
+ * use one set.  Mode 1 always uses one set, mode 2 uses two wherever the
+ * launch shape has room (bf16 d <= 128, fp32 Pass 2 with d <= 64).  The two
+ * forms sum in different orders, so their results differ by rounding; for a
+ * given mode, device and problem the result is deterministic.  Process-wide
+ * (all devices); not ordered against launches in flight.  Returns BOB_OK, or
+ * BOB_EINVAL for a mode outside 0..2. */
+int32_t bob_set_column_wave_sets(int32_t mode);
+
 #ifdef __cplusplus
 }
 #endif

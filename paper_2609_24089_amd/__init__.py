@@ -55,12 +55,22 @@ def load_library():
     lib.bob_status_string.restype = ctypes.c_char_p
     lib.bob_version.argtypes = []
     lib.bob_version.restype = ctypes.c_char_p
+    lib.bob_set_column_wave_sets.argtypes = [i32]
+    lib.bob_set_column_wave_sets.restype = i32
     _lib = lib
     return lib
 
 
 def status_string(rc):
     return load_library().bob_status_string(int(rc)).decode()
+
+
+def set_column_wave_sets(mode):
+    """bob_set_column_wave_sets: 0 automatic (default), 1 one wave set per
+    column block, 2 two wherever the launch shape has room."""
+    rc = load_library().bob_set_column_wave_sets(int(mode))
+    if rc != BOB_OK:
+        raise ValueError(f"bob_set_column_wave_sets({mode}): {status_string(rc)}")
 
 
 def _dtype_code(t):

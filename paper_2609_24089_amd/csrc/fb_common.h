@@ -313,11 +313,13 @@ constexpr int tile_loads() {
   return NTENS * Geo<T, D>::kBlocks / NW;
 }
 
+// w is the wave's index among the NW waves that share the copy.
 template <typename T, int D, int NW, int NTENS>
-__device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N) {
+__device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N,
+                                            int w = wave_id()) {
   using G = Geo<T, D>;
   constexpr int kBlockElems = 1024 / (int)sizeof(T);
-  const int l = lane_id(), w = wave_id();
+  const int l = lane_id();
   auto one = [&](const T* base, int t, int b) {
     int r, c;
     G::slot_source(b * 64 + l, r, c);
@@ -461,6 +463,63 @@ __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool ow
     __syncthreads();
     cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
   }
+}
+
+// Iteration space of a column-major kernel's streaming loop.  The streamed
+// side is the query tiles it_begin .. it_begin + nTh - 1 (under the causal
+// mask the tiles before it_begin lie entirely above the column block's
+// diagonal).  With kGQA it is those tiles of each of the grp query heads that
+// share key/value head bh, one head after another: nIt = grp * nTh flattened
+// iterations, flattened iteration i being tile it_begin + i % nTh of query
+// head bh * grp + i / nTh.  With KS wave sets, set ks takes flattened
+// iterations ks, ks + KS, ks + 2 KS, ...; every set runs the same number of
+// loop iterations (the loop's barriers are workgroup-wide), and an iteration
+// past the end (live() false) loads the last valid tile again and skips the
+// math, so each wave's count of outstanding copies is the same as on a live
+// iteration.
+template <bool kGQA, int KS>
+struct StreamSplit {
+  int it_begin, nTh, nIt, ks, bh, grp;
+  __device__ __forceinline__ int begin() const { return KS == 1 && !kGQA ? it_begin : 0; }
+  __device__ __forceinline__ int end(int nT) const { return KS == 1 ? (kGQA ? nIt : nT) : (nIt + KS - 1) / KS; }
+  __device__ __forceinline__ int flat(int it) const { return KS == 1 ? it : min(ks + KS * it, nIt - 1); }
+  __device__ __forceinline__ bool live(int it) const { return KS == 1 || ks + KS * it < nIt; }
+  __device__ __forceinline__ int qhead(int it) const { return kGQA ? bh * grp + flat(it) / nTh : bh; }
+  __device__ __forceinline__ int tile(int it) const {
+    if (KS == 1 && !kGQA) return it;
+    return it_begin + (kGQA ? flat(it) % nTh : flat(it));
+  }
+};
+
+// Two wave sets of one workgroup that accumulated the same stationary rows
+// over disjoint sets of streamed tiles: set 1 hands its fp32 accumulators x,
+// then y, to set 0 through LDS (buf: every wave's A*B 1 KB blocks, placed by
+// the wave's index wl within its set), and set 0 adds them, always in the
+// order set 0 + set 1.  Every wave of the workgroup calls it (it holds
+// barriers); buf may alias the tile ring once the streaming loop has ended
+// (its last barrier follows the last read and the last copy).
+template <int A, int B>
+__device__ __forceinline__ void merge_wave_sets(floatx4 (&x)[A][B], floatx4 (&y)[A][B], int ks, int wl,
+                                                floatx4 FB_LDS* buf) {
+  floatx4 FB_LDS* p = buf + wl * (A * B * 64) + lane_id();
+  auto one = [&](floatx4 (&acc)[A][B]) {
+    if (ks == 1) {
+#pragma unroll
+      for (int a = 0; a < A; ++a)
+#pragma unroll
+        for (int b = 0; b < B; ++b) p[(a * B + b) * 64] = acc[a][b];
+    }
+    __syncthreads();
+    if (ks == 0) {
+#pragma unroll
+      for (int a = 0; a < A; ++a)
+#pragma unroll
+        for (int b = 0; b < B; ++b) acc[a][b] += p[(a * B + b) * 64];
+    }
+  };
+  one(x);
+  __syncthreads();  // set 0 has read x before set 1 overwrites it with y
+  one(y);
 }
 
 // Streamed per-row fp32 scalars (L, D, alpha, E) for one tile, copied HBM ->

@@ -272,26 +272,33 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // ===========================================================================
 // First backward, column side: dV = P^T dO and dK = tau dS^T Q (eqs. 2-3).
 // Stationary: K, V rows.  Streamed: Q, dO tiles with their L and D.
+// KS wave sets of NW waves share the workgroup's column block and take the
+// streamed tiles round-robin, each with its own LDS ring; their partial sums
+// are added through LDS at the end (KS = 2 fills a CU when the grid has no
+// more workgroups than CUs).
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA>
-__global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS>
+__global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
     T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal, int grp) {
+  static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
-  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][2 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) T lds[KS][NSTAGE][2 * G::kTileElems];
   // raw L, D of NSTAGE tiles, and two slots of transformed ones:
   // T0 = -L log2e (the exponent offset), T1 = -D (the dP tile's start value)
-  __shared__ __attribute__((aligned(16))) float rawsc[NSTAGE][2 * kBS];
-  __shared__ __attribute__((aligned(16))) float tsc[2][2 * kBS];
+  __shared__ __attribute__((aligned(16))) float rawsc[KS][NSTAGE][2 * kBS];
+  __shared__ __attribute__((aligned(16))) float tsc[KS][2][2 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
-  const int col0 = rb * BC + wave_id() * 16 * MC;
+  const int ks = KS == 1 ? 0 : wave_id() / NW;       // wave set
+  const int wl = KS == 1 ? wave_id() : wave_id() % NW;  // wave within its set
+  const int col0 = rb * BC + wl * 16 * MC;
 
   u32x4 kf[MC][G::kChunks], vf[MC][G::kChunks];
 #pragma unroll
@@ -325,43 +332,38 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
 
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
-  // With kGQA the streamed side runs over the grp query heads that share
-  // this key/value head, one after another: iteration it is tile
-  // it_begin + it % nTh of query head bh * grp + it / nTh.  Without it the
-  // streamed rows are those of head bh.
   const int nTh = nT - it_begin;
-  auto qhead = [&](int it) { return kGQA ? bh * grp + it / nTh : bh; };
-  auto tile = [&](int it) { return kGQA ? it_begin + it % nTh : it; };
+  const StreamSplit<kGQA, KS> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp};
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 2>(), 1>(
-      kGQA ? 0 : it_begin, kGQA ? grp * nTh : nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
-        const int64_t qs = (int64_t)qhead(it) * N;
-        issue_scalar_pair((float FB_LDS*)rawsc[rs], L + qs, Dv + qs, tile(it) * kBS, N);
+        const int64_t qs = (int64_t)sp.qhead(it) * N;
+        issue_scalar_pair((float FB_LDS*)rawsc[ks][rs], L + qs, Dv + qs, sp.tile(it) * kBS, N);
       },
       [&](int it, int st) {
-        const int64_t qo = (int64_t)qhead(it) * N * D;
+        const int64_t qo = (int64_t)sp.qhead(it) * N * D;
         const T* const src[2] = {Q + qo, dO + qo};
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], tile(it) * kBS, N);
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N, wl);
       },
       [&](int it, int rs, int ts) {
         (void)it;
         if (l < kBS) {
-          const float FB_LDS* raw = (const float FB_LDS*)rawsc[rs];
-          float FB_LDS* t = (float FB_LDS*)tsc[ts];
+          const float FB_LDS* raw = (const float FB_LDS*)rawsc[ks][rs];
+          float FB_LDS* t = (float FB_LDS*)tsc[ks][ts];
           t[l] = -raw[l] * kLog2e;
           t[kBS + l] = -raw[kBS + l];
         }
       },
       [&](int it, int st, int ts, auto&& prep_next) {
-        const int s0 = tile(it) * kBS;
-        const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
+        const int s0 = sp.tile(it) * kBS;
+        const int mode = sp.live(it) ? tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0) : 0;
         if (mode == 0) {
           prep_next();
           return;
         }
-        const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
+        const T FB_LDS* Qs = (const T FB_LDS*)lds[ks][st];
         const T FB_LDS* dOs = Qs + G::kTileElems;
-        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ts];
+        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ks][ts];
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
           const floatx4 t1 = *(const floatx4 FB_LDS*)(Ts + kBS + 16 * sb + 4 * g);
@@ -406,6 +408,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_cols_kernel(
         }
         prep_next();
       });
+  if constexpr (KS == 2) {
+    static_assert(sizeof(lds) >= (size_t)NW * G::kNB * MC * 1024, "set merge buffer");
+    merge_wave_sets(dk, dv, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);
+    if (ks != 0) return;
+  }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
     const int col = col0 + 16 * mc + j;
@@ -754,28 +761,32 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 // rows.  Streamed: Q, U_Q, dO tiles with L, D, alpha, E.  Per tile:
 //   h = F - alpha, dS = P (dP - D), Pt = C + F (dP - D) - alpha dP,
 //   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
-// Writes Kt, Vt once; no atomics.
+// Writes Kt, Vt once; no atomics.  Wave sets (KS) as in the column side of
+// the first backward.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA>
-__global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS>
+__global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
     const float* __restrict__ alpha_in, const float* __restrict__ E_in,
     T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp) {
+  static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
   constexpr int BC = 16 * MC * NW;
-  __shared__ __attribute__((aligned(16))) T lds[NSTAGE][3 * G::kTileElems];
+  __shared__ __attribute__((aligned(16))) T lds[KS][NSTAGE][3 * G::kTileElems];
   // raw L, D, alpha, E of NSTAGE tiles, and two slots of transformed ones
-  __shared__ __attribute__((aligned(16))) float rawsc[NSTAGE][4 * kBS];
-  __shared__ __attribute__((aligned(16))) float tsc[2][4 * kBS];
+  __shared__ __attribute__((aligned(16))) float rawsc[KS][NSTAGE][4 * kBS];
+  __shared__ __attribute__((aligned(16))) float tsc[KS][2][4 * kBS];
 
   int bh, rb;
   map_block(nRB, total, bh, rb);
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
-  const int col0 = rb * BC + wave_id() * 16 * MC;
+  const int ks = KS == 1 ? 0 : wave_id() / NW;       // wave set
+  const int wl = KS == 1 ? wave_id() : wave_id() % NW;  // wave within its set
+  const int col0 = rb * BC + wl * 16 * MC;
 
   u32x4 kf[MC][G::kChunks], vf[MC][G::kChunks], ukf[MC][G::kChunks], uvf[MC][G::kChunks];
 #pragma unroll
@@ -825,31 +836,26 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
   const float inv_scale = 1.0f / scale;
-  // With kGQA the streamed side runs over the grp query heads that share
-  // this key/value head, one after another: iteration it is tile
-  // it_begin + it % nTh of query head bh * grp + it / nTh.  Without it the
-  // streamed rows are those of head bh.
   const int nTh = nT - it_begin;
-  auto qhead = [&](int it) { return kGQA ? bh * grp + it / nTh : bh; };
-  auto tile = [&](int it) { return kGQA ? it_begin + it % nTh : it; };
+  const StreamSplit<kGQA, KS> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp};
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 3>(), 2>(
-      kGQA ? 0 : it_begin, kGQA ? grp * nTh : nT, __builtin_amdgcn_readfirstlane(wave_id()) == 0,
+      sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
-        const int64_t qs = (int64_t)qhead(it) * N;
-        float FB_LDS* dst = (float FB_LDS*)rawsc[rs];
-        issue_scalar_pair(dst, L + qs, Dv + qs, tile(it) * kBS, N);
-        issue_scalar_pair(dst + 2 * kBS, alpha_in + qs, E_in + qs, tile(it) * kBS, N);
+        const int64_t qs = (int64_t)sp.qhead(it) * N;
+        float FB_LDS* dst = (float FB_LDS*)rawsc[ks][rs];
+        issue_scalar_pair(dst, L + qs, Dv + qs, sp.tile(it) * kBS, N);
+        issue_scalar_pair(dst + 2 * kBS, alpha_in + qs, E_in + qs, sp.tile(it) * kBS, N);
       },
       [&](int it, int st) {
-        const int64_t qo = (int64_t)qhead(it) * N * D;
+        const int64_t qo = (int64_t)sp.qhead(it) * N * D;
         const T* const src[3] = {Q + qo, UQ + qo, dO + qo};
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], tile(it) * kBS, N);
+        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N, wl);
       },
       [&](int it, int rs, int ts) {
         (void)it;
         if (l < kBS) {
-          const float FB_LDS* raw = (const float FB_LDS*)rawsc[rs];
-          float FB_LDS* t = (float FB_LDS*)tsc[ts];
+          const float FB_LDS* raw = (const float FB_LDS*)rawsc[ks][rs];
+          float FB_LDS* t = (float FB_LDS*)tsc[ks][ts];
           const float Lr = raw[l], Dr = raw[kBS + l], ar = raw[2 * kBS + l], Er = raw[3 * kBS + l];
           t[l] = -Lr * kLog2e;
           t[kBS + l] = -Dr;
@@ -858,16 +864,16 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
         }
       },
       [&](int it, int st, int ts, auto&& prep_next) {
-        const int s0 = tile(it) * kBS;
-        const int mode = tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0);
+        const int s0 = sp.tile(it) * kBS;
+        const int mode = sp.live(it) ? tile_mode_colmajor(s0, col0, col0 + 16 * MC - 1, N, causal != 0) : 0;
         if (mode == 0) {
           prep_next();
           return;
         }
-        const T FB_LDS* Qs = (const T FB_LDS*)lds[st];
+        const T FB_LDS* Qs = (const T FB_LDS*)lds[ks][st];
         const T FB_LDS* UQs = Qs + G::kTileElems;
         const T FB_LDS* dOs = UQs + G::kTileElems;
-        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ts];
+        const float FB_LDS* Ts = (const float FB_LDS*)tsc[ks][ts];
         // score tiles [s = query][t = key], started from the row terms
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
@@ -923,6 +929,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass2_kernel(
           }
         }
       });
+  if constexpr (KS == 2) {
+    static_assert(sizeof(lds) >= (size_t)NW * G::kNB * MC * 1024, "set merge buffer");
+    merge_wave_sets(aK, aV, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);
+    if (ks != 0) return;
+  }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
     const int col = col0 + 16 * mc + j;

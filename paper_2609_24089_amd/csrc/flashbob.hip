@@ -1,5 +1,6 @@
 // C ABI of libflashbob.so: argument validation and kernel dispatch.
 // The entry points are declared (and documented) in include/flashbob.h.
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 
@@ -117,6 +118,46 @@ Grid grid_for(const Problem& p, int rows_per_block, bool kv_heads = false) {
   return g;
 }
 
+// Compute units of the current device (0 if it cannot be read), read once per
+// device.
+int device_cus() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Column kernels (bwd cols, Pass 2) run two wave sets per workgroup when the
+// grid has no more workgroups than the device has CUs (few key/value heads
+// times few column blocks, e.g. multi-query attention): one 4-wave workgroup
+// per CU leaves half of its wave slots empty, and the two sets split the
+// streamed tiles instead.  That applies to shapes held to two waves per SIMD
+// (a one-wave shape already fills a CU with one workgroup), and needs the two
+// LDS rings (NTENS tiles and NSCAL row scalars per stage each) to fit a
+// workgroup's 160 KB and the sets' merge buffer to fit in the rings.
+// 0: two sets whenever the grid has no more workgroups than the device has
+// CUs; 1: never; 2: wherever the shape allows (bob_set_column_wave_sets).
+std::atomic<int> g_wave_sets{0};
+bool use_two_sets(int workgroups) {
+  const int mode = g_wave_sets.load(std::memory_order_relaxed);
+  if (mode == 1) return false;
+  if (mode == 2) return true;
+  return workgroups <= device_cus();
+}
+
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, int NTENS, int NSCAL>
+constexpr bool two_sets_fit() {
+  constexpr size_t ring = (size_t)NSTAGE * NTENS * Geo<T, D>::kTileElems * sizeof(T);
+  constexpr size_t scal = (size_t)(NSTAGE + 2) * NSCAL * kBS * sizeof(float);
+  return OCC == 2 && 2 * (ring + scal) <= 160 * 1024 &&
+         2 * ring >= (size_t)NW * Geo<T, D>::kNB * MC * 1024;
+}
+
 template <typename T, int D>
 int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V, void* O, float* L,
                    hipStream_t s) {
@@ -141,14 +182,22 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
   const Grid gc = grid_for(p, 16 * cc.mr * cc.nw, true);
-  if (group(p) == 1)
-    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, false>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
-                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal, group(p));
-  else
-    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true>), dim3(gc.total), dim3(64 * cc.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, L, (const float*)Dv, (T*)dK,
-                     (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal, group(p));
+  const bool two = use_two_sets(gc.total);
+  (void)hipGetLastError();
+  auto cols = [&](auto gqa, auto ks) {
+    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, decltype(gqa)::value, decltype(ks)::value>),
+                       dim3(gc.total), dim3(64 * cc.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V,
+                       (const T*)dO, L, (const float*)Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
+                       p.causal, group(p));
+  };
+  const bool gqa = group(p) != 1;
+  if constexpr (two_sets_fit<T, D, cc.mr, cc.nw, cc.occ, cc.st, 2, 2>()) {
+    if (two) {
+      gqa ? cols(std::true_type{}, std::integral_constant<int, 2>{}) : cols(std::false_type{}, std::integral_constant<int, 2>{});
+      return finish_launch();
+    }
+  }
+  gqa ? cols(std::true_type{}, std::integral_constant<int, 1>{}) : cols(std::false_type{}, std::integral_constant<int, 1>{});
   return finish_launch();
 }
 
@@ -211,15 +260,22 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
                      const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s) {
   constexpr Shape c = Cfg<T, D>::kP2;
   const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
+  const bool two = use_two_sets(g.total);
   (void)hipGetLastError();
-  if (group(p) == 1)
-    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, false>), dim3(g.total), dim3(64 * c.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
-                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
-  else
-    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, true>), dim3(g.total), dim3(64 * c.nw), 0, s,
-                     (const T*)Q, (const T*)K, (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK,
-                     (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
+  auto pass2 = [&](auto gqa, auto ks) {
+    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value>), dim3(g.total),
+                       dim3(64 * c.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
+                       (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N,
+                       g.nRB, g.total, p.scale, p.causal, group(p));
+  };
+  const bool gqa = group(p) != 1;
+  if constexpr (two_sets_fit<T, D, c.mr, c.nw, c.occ, c.st, 3, 4>()) {
+    if (two) {
+      gqa ? pass2(std::true_type{}, std::integral_constant<int, 2>{}) : pass2(std::false_type{}, std::integral_constant<int, 2>{});
+      return finish_launch();
+    }
+  }
+  gqa ? pass2(std::true_type{}, std::integral_constant<int, 1>{}) : pass2(std::false_type{}, std::integral_constant<int, 1>{});
   return finish_launch();
 }
 
@@ -396,5 +452,11 @@ const char* bob_status_string(int32_t status) {
 }
 
 const char* bob_version(void) { return "flashbob-gfx950 0.1"; }
+
+int32_t bob_set_column_wave_sets(int32_t mode) {
+  if (mode < 0 || mode > 2) return BOB_EINVAL;
+  fb::g_wave_sets.store(mode, std::memory_order_relaxed);
+  return BOB_OK;
+}
 
 }  // extern "C"

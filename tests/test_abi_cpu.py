@@ -185,3 +185,12 @@ def test_binding_checks_group_shapes():
     k2 = torch.zeros(1, 2, 9, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="must match the query side"):
         fb.attn_fwd_lse(q, k2, k2, 0.125)
+
+
+def test_column_wave_set_mode_is_validated(lib):
+    for bad in (-1, 3, 100):
+        assert lib.bob_set_column_wave_sets(bad) == fb.BOB_EINVAL
+    for ok in (1, 2, 0):
+        assert lib.bob_set_column_wave_sets(ok) == fb.BOB_OK
+    with pytest.raises(ValueError):
+        fb.set_column_wave_sets(5)
