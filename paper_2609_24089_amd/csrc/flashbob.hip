@@ -26,12 +26,12 @@ template <> struct Cfg<bf16, 32> {
 };
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{2, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
-  static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 3};
+  static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr Shape kFwd{1, 8, 2, 3}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
-  static constexpr Shape kP1{1, 8, 2, 3}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 3};
+  static constexpr Shape kFwd{1, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
+  static constexpr Shape kP1{1, 8, 2, 2}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 256> {
