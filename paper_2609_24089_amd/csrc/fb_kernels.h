@@ -19,7 +19,9 @@
 // reads key/value head bh / grp.  Row kernels run one workgroup per query
 // head row block; column kernels one per key/value head column block, and
 // stream the grp query heads of that key/value head one after another, so
-// their key-side outputs sum over the group with no atomics.
+// their key-side outputs sum over the group with no atomics.  On grids with
+// no more workgroups than CUs a column workgroup holds two wave sets that
+// split those streamed tiles and add their partial sums through LDS.
 #pragma once
 #include "fb_common.h"
 
