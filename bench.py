@@ -41,7 +41,7 @@ HBM_PEAK_GBS = 8000.0
 FLOP_COEF = {"fwd": 4, "bwd": 14, "pass1": 20, "pass2": 16}
 NOMINAL_BOB_COEF = 38
 
-KERNEL_SOURCES = ["fb_common.h", "fb_kernels.h", "flashbob.hip"]
+KERNEL_SOURCES = ["fb_common.h", "fb_kernels.h", "fb_launch.h", "flashbob.hip", "fb_passes_d128.hip"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 PEAK_N_FILE = os.path.join(ROOT, "profiles", "peak_n.json")
 
@@ -70,9 +70,12 @@ def code_tokens(text):
 
 
 def kernel_source_hash(read=None):
-    """Hash of the kernel sources' code (see code_tokens); `read(name)` may
-    supply the text of each file instead of the working tree."""
+    """Hash of the kernel sources' code (see code_tokens) and of the compiler
+    flags each translation unit is built with; `read(name)` may supply the
+    text of each file instead of the working tree."""
+    from paper_2609_24089_amd.build import HIPCC_FLAGS, SOURCES
     h = hashlib.sha256()
+    h.update(repr((HIPCC_FLAGS, SOURCES)).encode())
     for name in KERNEL_SOURCES:
         if read is None:
             with open(os.path.join(ROOT, "paper_2609_24089_amd", "csrc", name)) as f:

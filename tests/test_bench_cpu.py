@@ -32,9 +32,16 @@ def test_hash_follows_code():
     src = sources()
     base = bench.kernel_source_hash(lambda n: src[n])
     edited = dict(src)
-    edited["flashbob.hip"] = src["flashbob.hip"].replace("kP1{1, 8, 2, 3}", "kP1{1, 8, 2, 2}", 1)
-    assert edited["flashbob.hip"] != src["flashbob.hip"]
+    edited["fb_launch.h"] = src["fb_launch.h"].replace("kP1{1, 8, 2, 2}", "kP1{1, 8, 2, 3}", 1)
+    assert edited["fb_launch.h"] != src["fb_launch.h"]
     assert bench.kernel_source_hash(lambda n: edited[n]) != base
+
+
+def test_hash_follows_build_flags(monkeypatch):
+    from paper_2609_24089_amd import build
+    base = bench.kernel_source_hash()
+    monkeypatch.setattr(build, "SOURCES", [(n, []) for n, _ in build.SOURCES])
+    assert bench.kernel_source_hash() != base
 
 
 def test_code_tokens():
