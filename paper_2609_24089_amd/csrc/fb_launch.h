@@ -97,10 +97,12 @@ inline int32_t check_problem(const Problem& p, bool* empty) {
     return BOB_OK;
   }
   if (p.N > kMaxN) return BOB_EINVAL;
-  // grid size: heads x row blocks must fit a 32-bit grid (smallest block is 64 rows)
+  // 32-bit grid and loop counts: heads x row blocks (the smallest block is 64
+  // rows) sizes the grid, and a column kernel streams up to H/Hkv heads of
+  // ceil(N/32) tiles in one loop, so heads x 32-row tiles must fit an int
   const int64_t heads = p.B * p.H;
   if (p.B > INT32_MAX || p.H > INT32_MAX || heads > INT32_MAX) return BOB_EINVAL;
-  if (heads * ((p.N + 63) / 64) > INT32_MAX) return BOB_EINVAL;
+  if (heads * ((p.N + 31) / 32) > INT32_MAX) return BOB_EINVAL;
   return BOB_OK;
 }
 

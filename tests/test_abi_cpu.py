@@ -85,6 +85,8 @@ def test_rejects_bad_arguments_without_launching(lib, fn):
     assert call(lib, fn, ptr=0) == fb.BOB_EINVAL
     assert call(lib, fn, N=(1 << 30) + 1) == fb.BOB_EINVAL
     assert call(lib, fn, B=1 << 20, H=1 << 20) == fb.BOB_EINVAL
+    # heads x 32-row tiles past the int range (the column kernels' loop count)
+    assert call(lib, fn, H=1 << 10, N=1 << 26) == fb.BOB_EINVAL
     assert call(lib, fn, causal=2) == fb.BOB_EINVAL
     assert call(lib, fn, causal=-1) == fb.BOB_EINVAL
 
