@@ -117,9 +117,10 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
         threads = os.cpu_count() or 1
     slab = min(slab, w.N)
     rows, keys, dt, heads_used = 0, 0, 0.0, 0
+    group = w.H // w.kv_heads
     for b in range(w.B):
         for h in range(w.H):
-            mats = [as_f64(x_cpu[n][b, h]) for n in NAMES]
+            mats = [as_f64(x_cpu[n][b, h // group if n in ("K", "V", "UK", "UV") else h]) for n in NAMES]
             heads_used += 1
             for r0 in range(0, w.N, slab):
                 sel = np.arange(r0, min(w.N, r0 + slab))
@@ -180,14 +181,15 @@ class Path:
 
     def __init__(self, fb, torch, x, w, dev):
         self.fb, self.w, self.x = fb, w, x
-        Q = x["Q"]
+        Q, K = x["Q"], x["K"]
         rows_shape = (w.B, w.H, w.N)
         E_ = lambda: torch.empty_like(Q)
+        KE_ = lambda: torch.empty_like(K)   # key-side outputs: Hkv heads
         R_ = lambda: torch.empty(rows_shape, dtype=torch.float32, device=dev)
         self.O, self.L = E_(), R_()
-        self.dQ, self.dK, self.dV, self.D = E_(), E_(), E_(), R_()
+        self.dQ, self.dK, self.dV, self.D = E_(), KE_(), KE_(), R_()
         self.Qt, self.dOt, self.alpha, self.E = E_(), E_(), R_(), R_()
-        self.Kt, self.Vt = E_(), E_()
+        self.Kt, self.Vt = KE_(), KE_()
 
     def step(self, ev):
         fb, x, s, c = self.fb, self.x, self.w.scale, self.w.causal
@@ -274,8 +276,11 @@ def ablation(args, log):
     import torch
     import paper_2609_24089_amd as fb
     from workloads import WORKLOADS, workload_inputs
-    fb.load_library()
     w = WORKLOADS[args.workload]
+    if w.kv_heads != w.H:
+        sys.exit("--ablation: the three-pass control schedule is built for multi-head attention; "
+                 f"{w.name} shares key/value heads")
+    fb.load_library()
     dev = torch.device("cuda:0")
     x = {k: v.to(dev) for k, v in workload_inputs(w).items()}
     Q, K, V, dO, UQ, UK, UV = (x[n] for n in ("Q", "K", "V", "dO", "UQ", "UK", "UV"))
@@ -424,7 +429,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "scale": w.scale,
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "Hkv": w.kv_heads, "N": w.N, "d": w.d, "scale": w.scale,
                    "seed": w.seed, "qk_scale": w.qk_scale, "causal": w.causal},
         "pct_peak": round(100.0 * value / peak, 2),
         "bob_ms": {"median": round(bob_med, 4), "p20": round(q(bob_ms, 0.2), 4),

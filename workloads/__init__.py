@@ -30,6 +30,11 @@ class Workload:
     seed: int
     qk_scale: float = 1.0
     causal: bool = False  # the problem flag passed with these inputs (not part of the draw)
+    Hkv: int = 0          # key/value heads shared by the H query heads; 0 means H (multi-head)
+
+    @property
+    def kv_heads(self) -> int:
+        return self.Hkv or self.H
 
     @property
     def scale(self) -> float:
@@ -59,6 +64,11 @@ WORKLOADS = {
 for _d, _seed in ((32, 8), (64, 9), (128, 10), (256, 11)):
     _n = f"causal_bf16_b4h12_n4096_d{_d}"
     WORKLOADS[_n] = Workload(_n, 4, 12, 4096, _d, "bf16", _seed, causal=True)
+# Grouped key/value heads at the N=16K d=128 shape: 4 and 1 (multi-query) key/value heads for 16 query heads.
+for _n, _hkv, _seed, _causal in (("gqa_bf16_b1h16kv4_n16384_d128", 4, 12, False),
+                                 ("mqa_bf16_b1h16kv1_n16384_d128", 1, 13, False),
+                                 ("causal_mqa_bf16_b1h16kv1_n16384_d128", 1, 14, True)):
+    WORKLOADS[_n] = Workload(_n, 1, 16, 16384, 128, "bf16", _seed, 0.5, causal=_causal, Hkv=_hkv)
 
 
 def make_inputs(B, H, N, d, dtype="bf16", seed=0, qk_scale=1.0, device="cpu"):
@@ -75,21 +85,26 @@ def make_inputs(B, H, N, d, dtype="bf16", seed=0, qk_scale=1.0, device="cpu"):
     return out
 
 
-def make_gqa_inputs(B, H, Hkv, N, d, dtype="bf16", seed=0, device="cpu"):
+def make_gqa_inputs(B, H, Hkv, N, d, dtype="bf16", seed=0, device="cpu", qk_scale=1.0):
     """Grouped-query inputs: Q, dO, UQ with H heads and K, V, UK, UV with Hkv
     heads, drawn in the order of NAMES from one seeded generator as in
-    make_inputs (N(0,1) float32, then cast)."""
+    make_inputs (N(0,1) float32, Q and K times qk_scale, then cast)."""
     gen = torch.Generator(device="cpu")
     gen.manual_seed(int(seed))
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     out = {}
     for name in NAMES:
         heads = Hkv if name in ("K", "V", "UK", "UV") else H
-        out[name] = torch.randn((B, heads, N, d), generator=gen, dtype=torch.float32).to(tdt).to(device)
+        x = torch.randn((B, heads, N, d), generator=gen, dtype=torch.float32)
+        if name in ("Q", "K") and qk_scale != 1.0:
+            x = x * qk_scale
+        out[name] = x.to(tdt).to(device)
     return out
 
 
 def workload_inputs(w: Workload, device="cpu"):
+    if w.kv_heads != w.H:
+        return make_gqa_inputs(w.B, w.H, w.kv_heads, w.N, w.d, w.dtype, w.seed, device, w.qk_scale)
     return make_inputs(w.B, w.H, w.N, w.d, w.dtype, w.seed, w.qk_scale, device)
 
 
