@@ -115,6 +115,12 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    cpu_model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), cpu_model)
+    except OSError:  # pragma: no cover
+        pass
     slab = min(slab, w.N)
     rows, keys, dt, heads_used = 0, 0, 0.0, 0
     group = w.H // w.kv_heads
@@ -143,7 +149,8 @@ def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
         "kind": "oracle",
         "sample": (f"float64 oracle bob_rows on {rows} query rows ({slab}-row slabs over {heads_used} "
                    f"head(s)) of {w.name}: row-owned outputs Qt, dOt, alpha, E in {dt:.1f} s; rate counts "
-                   f"the Pass-1 FLOPs 22*d*(keys seen by those rows); BLAS threads={threads}, host cores={os.cpu_count()}"),
+                   f"the Pass-1 FLOPs 22*d*(keys seen by those rows); BLAS threads={threads}, host cores={os.cpu_count()}, "
+                   f"{cpu_model}"),
     }
 
 
@@ -409,6 +416,9 @@ def main():
         tf = FLOP_COEF[n] * unit / (mean_ms * 1e-3) / 1e12
         kern[n] = {"ms_mean": round(mean_ms, 4), "ms_median": round(statistics.median(per[n]), 4),
                    "tflops": round(tf, 2), "frac_peak": round(tf / peak, 4)}
+        kt = measured_traffic(n, w.name)
+        if kt is not None:   # HBM bytes per launch from the committed counters / this run's launch time
+            kern[n]["hbm_gbps"] = round(kt / (mean_ms * 1e-3) / 1e9, 1)
     dom = max(("pass1", "pass2"), key=lambda n: statistics.mean(per[n]))
     dom_ms = statistics.mean(per[dom])
     achieved = FLOP_COEF[dom] * unit / (dom_ms * 1e-3) / 1e12
