@@ -223,11 +223,6 @@ template <typename T, int D> struct Geo {
     }
   }
 
-  // score A-operand: row r, the lane group's chunk of MFMA step kk
-  static __device__ __forceinline__ u32x4 read_chunk(const T FB_LDS* X, int r, int kk) {
-    return *(const u32x4 FB_LDS*)(X + chunk_off(r, 4 * kk + (lane_id() >> 4)));
-  }
-
   // A-operand of the accumulate step: dims [dim0, dim0+16) x the 32 tile rows,
   // transposed; lane l gets rows {4g..4g+3, 16+4g..16+4g+3} (g = l >> 4) of
   // dim dim0 + (l & 15), matching the score tiles' row order.
