@@ -1,8 +1,9 @@
 """GPU parity of grouped key/value heads (GQA; MQA when Hkv = 1) against the
 float64 oracle `oracle.bob_gqa`: the whole path through the C ABI's grouped
 entry points (chosen by the binding from the tensor shapes), every output,
-dense and causal, ragged N, both dtypes and every head dim; and the autograd
-wrapper's Hessian-vector product with shared key/value heads."""
+dense and causal, ragged N, both dtypes and every head dim; the autograd
+wrapper's Hessian-vector product with shared key/value heads; and the
+benchmark's multi-query workloads at full size on sampled rows and columns."""
 import numpy as np
 import pytest
 import torch
@@ -94,3 +95,56 @@ def test_autograd_hvp_with_grouped_heads(causal):
     say("   errs", {kk: f"{vv:.2e}" for kk, vv in errs.items()})
     for kk, e in errs.items():
         assert e <= TOL["f32"], (kk, e)
+
+
+KV_SIDE = ("K", "V", "UK", "UV")
+
+
+@pytest.mark.parametrize("name", ["mqa_bf16_b1h16kv1_n16384_d128", "causal_mqa_bf16_b1h16kv1_n16384_d128"])
+def test_multi_query_at_full_size(name):
+    """The multi-query workloads of the benchmark (B1, 16 query heads sharing
+    one key/value head, N = 16384, d = 128), run as the benchmark runs them
+    (its column kernels then take the two-wave-set form).  Row-owned outputs
+    on 32 sampled query rows of every head against the oracle; column-owned
+    outputs (Kt, Vt, dK, dV) on 64 sampled key rows, against the oracle's
+    column slices summed over the 16 query heads, given the GPU's row scalars
+    (which the sampled-row check covers); the identities I1-I3, I5, I6 on the
+    full outputs."""
+    from tests.parity_util import check_identities
+    from workloads import WORKLOADS, workload_inputs
+    w = WORKLOADS[name]
+    G = w.H // w.kv_heads
+    say(f"[gqa] {w.name}: GPU path")
+    x = workload_inputs(w)
+    xd = {k: v.cuda() for k, v in x.items()}
+    import paper_2609_24089_amd as fb
+    out = fb.bob(*[xd[n] for n in NAMES], w.scale, causal=w.causal)
+    torch.cuda.synchronize()
+    head = lambda h: [as_f64(x[n][0, h // G if n in KV_SIDE else h]) for n in NAMES]
+    rng = np.random.default_rng(3001)
+    row_keys = ("Qt", "dOt", "alpha", "E", "O", "L", "D", "dQ")
+    got, want = {k: [] for k in row_keys}, {k: [] for k in row_keys}
+    for h in range(w.H):
+        rows = np.unique(np.concatenate([[0], rng.choice(w.N, size=32, replace=False)]))
+        ref = oracle.bob_rows(*head(h), w.scale, rows, causal=w.causal)
+        idx = torch.as_tensor(rows, device=out["Qt"].device)
+        for k in row_keys:
+            got[k].append(as_f64(out[k][0, h].index_select(0, idx)))
+            want[k].append(ref[k])
+    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in row_keys}
+    say("   sampled-row errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    cols = np.sort(np.random.default_rng(3002).choice(w.N, size=64, replace=False))
+    col_keys = ("Kt", "Vt", "dK", "dV")
+    acc = {k: 0.0 for k in col_keys}
+    for h in range(w.H):
+        rs = {k: as_f64(out[k][0, h]) for k in ("alpha", "E", "L", "D")}
+        ref = oracle.bob_cols(*head(h), w.scale, cols, rs["alpha"], rs["E"], rs["L"], rs["D"], causal=w.causal)
+        for k in col_keys:
+            acc[k] = acc[k] + ref[k]
+    idx = torch.as_tensor(cols, device=out["Kt"].device)
+    for k in col_keys:
+        errs[k] = nrel(as_f64(out[k][0, 0].index_select(0, idx)), acc[k])
+    say("   errs with sampled columns", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL["bf16"], (k, e)
+    check_identities(xd, out)
