@@ -30,10 +30,13 @@
  *          so every row sum runs over keys j <= i; the kernels skip tiles
  *          above the diagonal.  All four calls of one problem must use the
  *          same value.
- *  pointers  device pointers owned by the caller, 16-byte aligned.  The
- *          library allocates no memory and keeps no state.  Outputs must not
- *          alias inputs.
- *  stream  a hipStream_t passed as void* (NULL = the default stream).  Work
+ *  pointers  device pointers owned by the caller, 16-byte aligned, on the
+ *          current HIP device (the kernels run there).  The library
+ *          allocates no memory; its only state is the mode set by
+ *          bob_set_column_wave_sets and a per-device count of compute units.
+ *          Outputs must not alias inputs.
+ *  stream  a hipStream_t of the current device passed as void* (NULL = the
+ *          default stream).  Work
  *          is enqueued asynchronously; the call returns before it finishes.
  *          Calls that consume another call's outputs (attn_bwd after
  *          attn_fwd_lse, pass 2 after pass 1) must be ordered on one stream

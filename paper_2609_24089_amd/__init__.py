@@ -123,13 +123,20 @@ def _p(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream):
-    s = torch.cuda.current_stream() if stream is None else stream
-    return ctypes.c_void_p(s.cuda_stream)
+def _stream(stream, like):
+    """The stream to enqueue on: `stream`, or the current stream of the
+    tensors' device.  The library launches on the current HIP device, which
+    _call sets to the tensors' device, so the stream must belong to it too."""
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream(like.device).cuda_stream)
+    if stream.device != like.device:
+        raise ValueError(f"stream is on {stream.device} but the tensors are on {like.device}")
+    return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _call(fn, *args):
-    rc = fn(*args)
+def _call(like, fn, *args):
+    with torch.cuda.device(like.device):
+        rc = fn(*args)
     if rc != BOB_OK:
         raise RuntimeError(status_string(rc))
 
@@ -148,11 +155,11 @@ def attn_fwd_lse(Q, K, V, scale, causal=False, out=None, stream=None):
     _check_mats(Q, O)
     _check_rows(Q.shape, L)
     lib = load_library()
-    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(L), _stream(stream, Q))
     if Hkv == H:
-        _call(lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_fwd_lse, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
     else:
-        _call(lib.attn_fwd_lse_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_fwd_lse_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
     return O, L
 
 
@@ -167,11 +174,11 @@ def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
     _check_mats(K, dK, dV)
     _check_rows(Q.shape, D)
     lib = load_library()
-    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream, Q))
     if Hkv == H:
-        _call(lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
     else:
-        _call(lib.attn_bwd_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_bwd_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
     return dQ, dK, dV, D
 
 
@@ -192,11 +199,11 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal=False
     _check_rows(Q.shape, alpha, E)
     lib = load_library()
     ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D),
-            None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream))
+            None if dQ is None else _p(dQ), _p(Qt), _p(dOt), _p(alpha), _p(E), _stream(stream, Q))
     if Hkv == H:
-        _call(lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_bob_pass1_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
     else:
-        _call(lib.attn_bob_pass1_rows_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
+        _call(Q, lib.attn_bob_pass1_rows_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
               *ptrs)
     return Qt, dOt, alpha, E
 
@@ -211,11 +218,11 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
     _check_mats(K, Kt, Vt)
     lib = load_library()
     ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
-            _p(Kt), _p(Vt), _stream(stream))
+            _p(Kt), _p(Vt), _stream(stream, Q))
     if Hkv == H:
-        _call(lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
     else:
-        _call(lib.attn_bob_pass2_cols_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
+        _call(Q, lib.attn_bob_pass2_cols_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
               *ptrs)
     return Kt, Vt
 
@@ -227,8 +234,8 @@ def attn_bob3_alpha_rows(Q, K, gdQ, gdK, L, scale, causal=False, out=None, strea
     alpha = _rows_empty(Q.shape, Q) if out is None else out
     _check_rows(Q.shape, alpha)
     lib = load_library()
-    _call(lib.attn_bob3_alpha_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
-          _p(Q), _p(K), _p(gdQ), _p(gdK), _p(L), _p(alpha), _stream(stream))
+    _call(Q, lib.attn_bob3_alpha_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
+          _p(Q), _p(K), _p(gdQ), _p(gdK), _p(L), _p(alpha), _stream(stream, Q))
     return alpha
 
 
@@ -242,9 +249,9 @@ def attn_bob3_rows(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, scale, causal=False,
     _check_mats(Q, Qt, dOt)
     _check_rows(Q.shape, E)
     lib = load_library()
-    _call(lib.attn_bob3_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
+    _call(Q, lib.attn_bob3_rows, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)),
           _p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha),
-          _p(Qt), _p(dOt), _p(E), _stream(stream))
+          _p(Qt), _p(dOt), _p(E), _stream(stream, Q))
     return Qt, dOt, E
 
 
