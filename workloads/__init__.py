@@ -1,9 +1,11 @@
 """Seeded synthetic inputs for attention BoB (shared by tests, bench and smoke).
 
 This module holds no arithmetic of the method: it only draws the seven
-[B, H, N, d] input tensors (Q, K, V, dO and the cotangents U_Q, U_K, U_V on
-the first-backward outputs) and names the workload shapes.  Both the HIP
-path and the float64 oracle consume the exact values it returns.
+input tensors (Q, K, V, dO and the cotangents U_Q, U_K, U_V on the
+first-backward outputs), all [B, H, N, d] or, for workloads with shared
+key/value heads, K, V, U_K, U_V with Hkv heads, and names the workload
+shapes.  Both the HIP path and the float64 oracle consume the exact values
+it returns.
 
 Recipe (the same for every workload): a CPU ``torch.Generator`` seeded with
 ``seed`` draws float32 standard normals of shape [B, H, N, d] in the order
