@@ -454,7 +454,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
 // ===========================================================================
 enum Pass1Form : int { kSixAcc = 0, kWithDQ = 1, kAlphaGiven = 2 };
 
-template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm, int DSPLIT>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm, int DSPLIT, bool kPF>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
@@ -581,16 +581,31 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     }
   };
   // accumulate: Acc^T[dim][t] += X^T[dim][s] T^T[s][t]
-  auto accumulate = [&](const T FB_LDS* Ks) {
-    const T FB_LDS* Vs = Ks + G::kTileElems;
-    const T FB_LDS* UKs = Vs + G::kTileElems;
-    const T FB_LDS* UVs = UKs + G::kTileElems;
+  // With kPF the step's transposed operand fragments are read one 16-dim
+  // block ahead of the MFMAs that use them (block 0 before the elementwise
+  // step), so the LDS latency of each block's reads overlaps the previous
+  // block's MFMAs; it costs 16 registers (4 fragments).
+  using AF = typename E::AFrag;
+  auto load_frags = [&](const T FB_LDS* Ks, int nb, AF (&f)[4]) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) f[t] = G::load_afrag(Ks + t * G::kTileElems, 16 * (nb0 + nb));
+  };
+  auto accumulate = [&](const T FB_LDS* Ks, AF (&cur)[4]) {
 #pragma unroll
     for (int nb = 0; nb < kNBh; ++nb) {
-      const typename E::AFrag ak = G::load_afrag(Ks, 16 * (nb0 + nb));
-      const typename E::AFrag av = G::load_afrag(Vs, 16 * (nb0 + nb));
-      const typename E::AFrag auk = G::load_afrag(UKs, 16 * (nb0 + nb));
-      const typename E::AFrag auv = G::load_afrag(UVs, 16 * (nb0 + nb));
+      AF ak, av, auk, auv;
+      if constexpr (kPF) {
+        ak = cur[0];
+        av = cur[1];
+        auk = cur[2];
+        auv = cur[3];
+        if (nb + 1 < kNBh) load_frags(Ks, nb + 1, cur);
+      } else {
+        ak = G::load_afrag(Ks, 16 * (nb0 + nb));
+        av = G::load_afrag(Ks + G::kTileElems, 16 * (nb0 + nb));
+        auk = G::load_afrag(Ks + 2 * G::kTileElems, 16 * (nb0 + nb));
+        auv = G::load_afrag(Ks + 3 * G::kTileElems, 16 * (nb0 + nb));
+      }
 #pragma unroll
       for (int mb = 0; mb < MR; ++mb) {
         aB[nb][mb] = E::mma_acc(ak, fP[mb], aB[nb][mb]);
@@ -621,9 +636,11 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
           for (int mb = 0; mb < MR; ++mb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) s[sb][mb][r] = __builtin_fmaf(s[sb][mb][r], c, -lb[mb]);
+        AF f0[4];
+        if constexpr (kPF) load_frags(Ks, 0, f0);
         if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
         elementwise();
-        accumulate(Ks);
+        accumulate(Ks, f0);
       });
 
   // epilogue (eq. 8; for kAlphaGiven the delayed E correction alone)
@@ -766,7 +783,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 // Writes Kt, Vt once; no atomics.  Wave sets (KS) as in the column side of
 // the first backward.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kPF>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
@@ -916,13 +933,31 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
 #pragma unroll
             for (int r = 0; r < 4; ++r) s[sb][mc][r] = __builtin_fmaf(s[sb][mc][r], c, t0[r]);
         }
+        // with kPF the accumulate operands are read one 16-dim block ahead
+        // of their MFMAs, as in Pass 1
+        typename E::AFrag cur[3];
+        if constexpr (kPF) {
+#pragma unroll
+          for (int t = 0; t < 3; ++t) cur[t] = G::load_afrag(Qs + t * G::kTileElems, 0);
+        }
         if (mode == 2) mask_tile<false>(s, s0, col0 + j, N, causal != 0);
         elementwise();
 #pragma unroll
         for (int nb = 0; nb < G::kNB; ++nb) {
-          const typename E::AFrag aq = G::load_afrag(Qs, 16 * nb);
-          const typename E::AFrag auq = G::load_afrag(UQs, 16 * nb);
-          const typename E::AFrag ado = G::load_afrag(dOs, 16 * nb);
+          typename E::AFrag aq, auq, ado;
+          if constexpr (kPF) {
+            aq = cur[0];
+            auq = cur[1];
+            ado = cur[2];
+            if (nb + 1 < G::kNB) {
+#pragma unroll
+              for (int t = 0; t < 3; ++t) cur[t] = G::load_afrag(Qs + t * G::kTileElems, 16 * (nb + 1));
+            }
+          } else {
+            aq = G::load_afrag(Qs, 16 * nb);
+            auq = G::load_afrag(UQs, 16 * nb);
+            ado = G::load_afrag(dOs, 16 * nb);
+          }
 #pragma unroll
           for (int mc = 0; mc < MC; ++mc) {
             aV[nb][mc] = E::mma_acc(ado, fPh[mc], aV[nb][mc]);

@@ -19,9 +19,10 @@ namespace fb {
 // blocks per wave, NW = waves per workgroup (a workgroup owns 16*MR*NW
 // stationary rows), OCC = waves per SIMD the register budget is held to, ST =
 // LDS pipeline stages (tiles in flight + 1), DS = workgroups that share one
-// row block, each accumulating 1/DS of the head dims (Pass 1 only).
+// row block, each accumulating 1/DS of the head dims (Pass 1 only), PF = 1 to
+// read the accumulate operands one block ahead (Pass 1 and Pass 2).
 struct Shape {
-  int mr, nw, occ, st, ds = 1;
+  int mr, nw, occ, st, ds = 1, pf = 0;
 };
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 32> {
@@ -36,7 +37,7 @@ template <> struct Cfg<bf16, 64> {
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{1, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
-  static constexpr Shape kP1{1, 8, 2, 2}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2};
+  static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 256> {
@@ -201,7 +202,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   if (dQ != nullptr) {
     constexpr Shape c = Cfg<T, D>::kP1;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ, c.ds>), dim3(g.total, c.ds),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ, c.ds, c.pf != 0>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -209,7 +210,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc, c.ds>), dim3(g.total, c.ds),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc, c.ds, c.pf != 0>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -238,7 +239,7 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
   constexpr Shape c = Cfg<T, D>::kP1;
   const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds>), dim3(g.total, c.ds),
+  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds, c.pf != 0>), dim3(g.total, c.ds),
                      dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)nullptr,
                      (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr, alpha,
                      (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
@@ -254,7 +255,7 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
   const bool two = use_two_sets(g.total);
   (void)hipGetLastError();
   auto pass2 = [&](auto gqa, auto ks) {
-    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value>), dim3(g.total),
+    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value, c.pf != 0>), dim3(g.total),
                        dim3(64 * c.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
                        (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N,
                        g.nRB, g.total, p.scale, p.causal, group(p));

@@ -32,7 +32,7 @@ def test_hash_follows_code():
     src = sources()
     base = bench.kernel_source_hash(lambda n: src[n])
     edited = dict(src)
-    edited["fb_launch.h"] = src["fb_launch.h"].replace("kP1{1, 8, 2, 2}", "kP1{1, 8, 2, 3}", 1)
+    edited["fb_launch.h"] = src["fb_launch.h"].replace("kP1{1, 8,", "kP1{1, 4,", 1)
     assert edited["fb_launch.h"] != src["fb_launch.h"]
     assert bench.kernel_source_hash(lambda n: edited[n]) != base
 
