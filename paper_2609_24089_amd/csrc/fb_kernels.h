@@ -907,23 +907,44 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
             cc[sb][mc] = t3;
           }
         }
+        // one score step: the five contractions of chunk kk of sub-block sb
+        auto score_step = [&](int sb, int kk, u32x4 aq, u32x4 auq, u32x4 ado) {
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int kk = 0; kk < G::kChunks; ++kk) {
-            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-            const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
-            const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
-            const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
-#pragma unroll
-            for (int mc = 0; mc < MC; ++mc) {
-              s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
-              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP - D
-              f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // (U_Q K^T
-              f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       //  + Q U_K^T) - alpha / tau
-              cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C - (alpha D + E)
-            }
+          for (int mc = 0; mc < MC; ++mc) {
+            s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);        // S = Q K^T
+            dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);     // dP - D
+            f[sb][mc] = E::mma_chunk(auq, kf[mc][kk], f[sb][mc]);       // (U_Q K^T
+            f[sb][mc] = E::mma_chunk(aq, ukf[mc][kk], f[sb][mc]);       //  + Q U_K^T) - alpha / tau
+            cc[sb][mc] = E::mma_chunk(ado, uvf[mc][kk], cc[sb][mc]);    // C - (alpha D + E)
           }
+        };
+        auto read_step = [&](int sb, int kk, u32x4 (&o)[3]) {
+          const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+          o[0] = *(const u32x4 FB_LDS*)(Qs + off);
+          o[1] = *(const u32x4 FB_LDS*)(UQs + off);
+          o[2] = *(const u32x4 FB_LDS*)(dOs + off);
+        };
+        if constexpr (kPF) {
+          // operands of step st + 1 are read before the MFMAs of step st
+          constexpr int kSteps = 2 * G::kChunks;
+          u32x4 nx[3];
+          read_step(0, 0, nx);
+#pragma unroll
+          for (int st = 0; st < kSteps; ++st) {
+            const u32x4 aq = nx[0], auq = nx[1], ado = nx[2];
+            if (st + 1 < kSteps) read_step((st + 1) / G::kChunks, (st + 1) % G::kChunks, nx);
+            score_step(st / G::kChunks, st % G::kChunks, aq, auq, ado);
+          }
+        } else {
+#pragma unroll
+          for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int kk = 0; kk < G::kChunks; ++kk) {
+              u32x4 a[3];
+              read_step(sb, kk, a);
+              score_step(sb, kk, a[0], a[1], a[2]);
+            }
+        }
         prep_next();
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
