@@ -276,7 +276,7 @@ def peak_n_sweep(args, log):
 def ablation(args, log):
     """The schedule ablation (App. "Three-pass versus two-pass", Table 7): on
     one workload, the median time of the BoB passes under (a) the two-pass
-    schedule as this build runs it (Pass 1 with dQ), (b) the two-pass schedule
+    schedule as the library runs it (Pass 1 with dQ), (b) the two-pass schedule
     with the six accumulators of Prop. 3.1 and (c) the three-pass control
     schedule (alpha sweep, row sweep, column pass).  Interleaved repetitions
     on the same resident inputs; prints one JSON line."""
@@ -355,7 +355,7 @@ def main():
                     help="time the two-pass and three-pass schedules on --workload instead")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the library runs on one GPU only; --gpus must be 1",
                           "gpus_requested": args.gpus}))
         sys.exit(2)
 
@@ -446,7 +446,7 @@ def main():
                    "p80": round(q(bob_ms, 0.8), 4)},
         "bob_tflops_min_count": round(24.0 * unit / (bob_med * 1e-3) / 1e12, 2),
         "bob_tflops_executed": round((FLOP_COEF["pass1"] + FLOP_COEF["pass2"]) * unit / (bob_med * 1e-3) / 1e12, 2),
-        "flop_count": f"value counts 38*B*H*{nsq}*d (the paper's 19 tile contractions per Alg. 2); this build "
+        "flop_count": f"value counts 38*B*H*{nsq}*d (the paper's 19 tile contractions per Alg. 2); the kernels "
                       f"executes 36 (Pass 1 takes dQ and skips R); bob_tflops_executed uses 36, "
                       f"bob_tflops_min_count 24",
         "step_tflops": round(step_flops / (wall / args.steps) / 1e12, 2),
