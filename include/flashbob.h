@@ -32,8 +32,10 @@
  *          same value.
  *  pointers  device pointers owned by the caller, 16-byte aligned, on the
  *          current HIP device (the kernels run there).  The library
- *          allocates no memory; its only state is the mode set by
- *          bob_set_column_wave_sets and a per-device count of compute units.
+ *          allocates no memory (attn_bob_pass2_cols_gqa_ws takes its
+ *          workspace from the caller); its only state is the modes set by
+ *          bob_set_column_wave_sets and bob_set_column_split and a
+ *          per-device count of compute units.
  *          Outputs must not alias inputs.
  *  stream  a hipStream_t of the current device passed as void* (NULL = the
  *          default stream).  Work
@@ -140,6 +142,37 @@ int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
                                 const float* L, const float* D, const float* alpha, const float* E, void* Kt,
                                 void* Vt, void* stream);
 
+/* Pass 2 with each key/value column block split over several workgroups,
+ * for grids too small to fill the device.  Under the causal mask a column
+ * block's work is proportional to the query tiles at or below its diagonal,
+ * so with few key/value heads (e.g. multi-query attention) the first blocks
+ * would set the time; split, every part takes an equal share of its block's
+ * (query head, query tile) iterations and stores fp32 partial Kt and Vt to
+ * `workspace`, and a second kernel on the same stream adds the parts in
+ * part order and writes Kt, Vt.
+ * Arguments as attn_bob_pass2_cols_gqa, plus:
+ *  workspace, workspace_bytes  device memory owned by the caller, 16-byte
+ *          aligned, of at least bob_pass2_workspace_bytes() bytes for this
+ *          problem; it needs no initial contents and holds nothing useful
+ *          afterwards.  It must not be reused before the call's kernels have
+ *          finished on `stream`.
+ * When bob_pass2_workspace_bytes() is 0 the call runs the unsplit kernels
+ * and ignores workspace (it may be NULL).  Otherwise a NULL, misaligned or
+ * too small workspace gives BOB_EINVAL.  Split and unsplit results differ by
+ * the order of the fp32 sums; each is deterministic. */
+int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                   float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                   const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                   const float* L, const float* D, const float* alpha, const float* E, void* Kt,
+                                   void* Vt, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes attn_bob_pass2_cols_gqa_ws needs for this problem on the
+ * current device under the current bob_set_column_split mode: 0 when it
+ * would not split (and for an empty or invalid problem, which that call
+ * reports), else parts x 2 x B x Hkv x N x d x 4. */
+int64_t bob_pass2_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                  int32_t causal);
+
 /* Three-pass control schedule (App. "Three-pass versus two-pass" and the
  * three-pass overlay of App. "Dependency graphs"): the schedule that the
  * affine fusion of Prop. 3.1 improves on, kept for the 2- vs 3-pass ablation
@@ -187,6 +220,14 @@ const char* bob_version(void);
  * (all devices); not ordered against launches in flight.  Returns BOB_OK, or
  * BOB_EINVAL for a mode outside 0..2. */
 int32_t bob_set_column_wave_sets(int32_t mode);
+
+/* How many workgroups attn_bob_pass2_cols_gqa_ws gives each column block.
+ * 0 (default): automatic, from the column grid, the device's compute units
+ * and the mask; 1: never split; 2..8: always that many parts.  Process-wide
+ * (all devices); read by bob_pass2_workspace_bytes and by the call itself,
+ * which must see the same mode.  Returns BOB_OK, or BOB_EINVAL for a value
+ * outside 0..8. */
+int32_t bob_set_column_split(int32_t parts);
 
 #ifdef __cplusplus
 }

@@ -57,6 +57,12 @@ def load_library():
     lib.bob_version.restype = ctypes.c_char_p
     lib.bob_set_column_wave_sets.argtypes = [i32]
     lib.bob_set_column_wave_sets.restype = i32
+    lib.bob_set_column_split.argtypes = [i32]
+    lib.bob_set_column_split.restype = i32
+    lib.bob_pass2_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32]
+    lib.bob_pass2_workspace_bytes.restype = i64
+    lib.attn_bob_pass2_cols_gqa_ws.argtypes = common_gqa + [vp] * 13 + [vp, i64] + [vp]
+    lib.attn_bob_pass2_cols_gqa_ws.restype = i32
     _lib = lib
     return lib
 
@@ -71,6 +77,14 @@ def set_column_wave_sets(mode):
     rc = load_library().bob_set_column_wave_sets(int(mode))
     if rc != BOB_OK:
         raise ValueError(f"bob_set_column_wave_sets({mode}): {status_string(rc)}")
+
+
+def set_column_split(parts):
+    """bob_set_column_split: 0 automatic (default), 1 never split a Pass 2
+    column block over workgroups, 2..8 always split it into that many."""
+    rc = load_library().bob_set_column_split(int(parts))
+    if rc != BOB_OK:
+        raise ValueError(f"bob_set_column_split({parts}): {status_string(rc)}")
 
 
 def _dtype_code(t):
@@ -217,13 +231,25 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
     Kt, Vt = out
     _check_mats(K, Kt, Vt)
     lib = load_library()
+    code, c = _dtype_code(Q), int(bool(causal))
     ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
-            _p(Kt), _p(Vt), _stream(stream, Q))
-    if Hkv == H:
-        _call(Q, lib.attn_bob_pass2_cols, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+            _p(Kt), _p(Vt))
+    st = _stream(stream, Q)
+    with torch.cuda.device(Q.device):
+        nbytes = lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, c)
+    if nbytes > 0:
+        # column blocks split over workgroups: fp32 partial sums in a
+        # workspace from torch's allocator, kept from reuse until the
+        # kernels on `stream` are done
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=Q.device)
+        if stream is not None:
+            ws.record_stream(stream)
+        _call(Q, lib.attn_bob_pass2_cols_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _p(ws), nbytes,
+              st)
+    elif Hkv == H:
+        _call(Q, lib.attn_bob_pass2_cols, code, B, H, N, d, float(scale), c, *ptrs, st)
     else:
-        _call(Q, lib.attn_bob_pass2_cols_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)),
-              *ptrs)
+        _call(Q, lib.attn_bob_pass2_cols_gqa, code, B, H, Hkv, N, d, float(scale), c, *ptrs, st)
     return Kt, Vt
 
 

@@ -471,13 +471,23 @@ __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool ow
 // loop iterations (the loop's barriers are workgroup-wide), and an iteration
 // past the end (live() false) loads the last valid tile again and skips the
 // math, so each wave's count of outstanding copies is the same as on a live
-// iteration.
-template <bool kGQA, int KS>
+// iteration.  With kParts the column block is split over nparts workgroups
+// (one wave set each): part p takes flattened iterations p, p + nparts, ...,
+// and its loop simply runs that many iterations (none if p >= nIt).
+template <bool kGQA, int KS, bool kParts = false>
 struct StreamSplit {
+  static_assert(!kParts || (KS == 1 && kGQA), "a split column block runs one wave set on the grouped loop");
   int it_begin, nTh, nIt, ks, bh, grp;
+  int part = 0, nparts = 1;
   __device__ __forceinline__ int begin() const { return KS == 1 && !kGQA ? it_begin : 0; }
-  __device__ __forceinline__ int end(int nT) const { return KS == 1 ? (kGQA ? nIt : nT) : (nIt + KS - 1) / KS; }
-  __device__ __forceinline__ int flat(int it) const { return KS == 1 ? it : min(ks + KS * it, nIt - 1); }
+  __device__ __forceinline__ int end(int nT) const {
+    if (kParts) return (nIt - part + nparts - 1) / nparts;
+    return KS == 1 ? (kGQA ? nIt : nT) : (nIt + KS - 1) / KS;
+  }
+  __device__ __forceinline__ int flat(int it) const {
+    if (kParts) return part + nparts * it;
+    return KS == 1 ? it : min(ks + KS * it, nIt - 1);
+  }
   __device__ __forceinline__ bool live(int it) const { return KS == 1 || ks + KS * it < nIt; }
   __device__ __forceinline__ int qhead(int it) const { return kGQA ? bh * grp + flat(it) / nTh : bh; }
   __device__ __forceinline__ int tile(int it) const {

@@ -788,15 +788,20 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 //   h = F - alpha, dS = P (dP - D), Pt = C + F (dP - D) - alpha dP,
 //   St = P (Pt - E);  Vt += (P h)^T dO,  Kt += tau (St^T Q + dS^T U_Q).
 // Writes Kt, Vt once; no atomics.  Wave sets (KS) as in the column side of
-// the first backward.
+// the first backward.  With kParts each column block is split over nparts
+// workgroups, which store fp32 partial sums of Kt / tau and Vt / tau to
+// parts_out ([nparts][2][B*Hkv][N][d]; bob_column_parts_reduce_kernel adds
+// them); the grid then holds total * nparts jobs, heaviest column block first.
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kPF>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kPF,
+          bool kParts = false>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
     const float* __restrict__ alpha_in, const float* __restrict__ E_in,
-    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp) {
+    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp,
+    float* __restrict__ parts_out = nullptr, int nparts = 1) {
   static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
@@ -818,8 +823,20 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   auto& rawsc = sm.rawsc;
   auto& tsc = sm.tsc;
 
-  int bh, rb;
-  map_block(nRB, total, bh, rb);
+  int bh, rb, part = 0;
+  if constexpr (kParts) {
+    // job = (rb * heads + bh) * nparts + part: under the causal mask block rb
+    // holds work in proportion to the tiles at or below its diagonal, so the
+    // jobs run heaviest first, and consecutive jobs (which go to different
+    // XCDs) carry similar work
+    const int heads = total / nRB, job = blockIdx.x;
+    rb = job / (heads * nparts);
+    const int rest = job - rb * heads * nparts;
+    bh = rest / nparts;
+    part = rest - bh * nparts;
+  } else {
+    map_block(nRB, total, bh, rb);
+  }
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int ks = KS == 1 ? 0 : wave_id() / NW;       // wave set
@@ -875,7 +892,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   const int it_begin = causal ? (rb * BC) / kBS : 0;
   const float inv_scale = 1.0f / scale;
   const int nTh = nT - it_begin;
-  const StreamSplit<kGQA, KS> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp};
+  const StreamSplit<kGQA, KS, kParts> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp, part, nparts};
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 3>(), 2>(
       sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
@@ -1011,6 +1028,26 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     merge_wave_sets(aK, aV, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);
     if (ks != 0) return;
   }
+  if constexpr (kParts) {
+    // every part stores all of its rows, zeros included, so the reduction
+    // needs no cleared buffer
+    const int64_t plane = (int64_t)(total / nRB) * N * D;
+    float* pk = parts_out + 2 * (int64_t)part * plane;
+    float* pv = pk + plane;
+#pragma unroll
+    for (int mc = 0; mc < MC; ++mc) {
+      const int col = col0 + 16 * mc + j;
+      if (col < N) {
+#pragma unroll
+        for (int nb = 0; nb < G::kNB; ++nb) {
+          const int64_t off = hoff + (int64_t)col * D + 16 * nb + 4 * g;
+          *(floatx4*)(pk + off) = aK[nb][mc];
+          *(floatx4*)(pv + off) = aV[nb][mc];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
     const int col = col0 + 16 * mc + j;
@@ -1022,6 +1059,24 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
         E::store4(Vt + off, aV[nb][mc] * scale);
       }
     }
+  }
+}
+
+// Sum of the nparts fp32 partial Kt / tau and Vt / tau planes of a split
+// Pass 2 (plane elements each, laid out [nparts][2][plane]), in part order,
+// times scale, rounded to the output type.  plane is a multiple of 4.
+template <typename T>
+__global__ __launch_bounds__(256) void bob_column_parts_reduce_kernel(const float* __restrict__ parts, int nparts,
+                                                                      int64_t plane, float scale,
+                                                                      T* __restrict__ Kt, T* __restrict__ Vt) {
+  using E = Elt<T>;
+  const int64_t n4 = plane / 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < 2 * n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const int t = i < n4 ? 0 : 1;
+    const int64_t off = 4 * (i - t * n4);
+    floatx4 acc = *(const floatx4*)(parts + t * plane + off);
+    for (int q = 1; q < nparts; ++q) acc += *(const floatx4*)(parts + (2 * (int64_t)q + t) * plane + off);
+    E::store4((t == 0 ? Kt : Vt) + off, acc * scale);
   }
 }
 

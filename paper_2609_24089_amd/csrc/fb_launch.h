@@ -5,6 +5,7 @@
 // scheduler (see that file), and every other unit refers to them through the
 // extern template declarations at the end.
 #pragma once
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdint>
@@ -249,11 +250,24 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
 template <typename T, int D>
 int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
                      const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
-                     const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s) {
+                     const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s,
+                     float* parts_ws = nullptr, int parts = 1) {
   constexpr Shape c = Cfg<T, D>::kP2;
   const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const bool two = use_two_sets(g.total);
   (void)hipGetLastError();
+  if (parts > 1) {
+    // each column block split over `parts` workgroups, then one reduction
+    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, true, 1, c.pf != 0, true>),
+                       dim3(g.total * parts), dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
+                       (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt,
+                       (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p), parts_ws, parts);
+    const int64_t plane = p.B * p.Hkv * p.N * p.d;
+    const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
+    hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
+                       parts, plane, p.scale, (T*)Kt, (T*)Vt);
+    return finish_launch();
+  }
+  const bool two = use_two_sets(g.total);
   auto pass2 = [&](auto gqa, auto ks) {
     hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value, c.pf != 0>), dim3(g.total),
                        dim3(64 * c.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
@@ -271,12 +285,30 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
   return finish_launch();
 }
 
+// How many workgroups share a Pass 2 column block (1: no split), from the
+// mode set by bob_set_column_split, the column grid and the mask.
+int column_parts(int workgroups, bool causal);
+
+template <typename T, int D>
+int pass2_parts(const Problem& p) {
+  constexpr Shape c = Cfg<T, D>::kP2;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
+  const int parts = column_parts(g.total, p.causal != 0);
+  return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
+}
+
+// fp32 workspace of a split Pass 2: parts x {Kt, Vt} x B*Hkv*N*d.
+inline int64_t pass2_workspace_bytes(const Problem& p, int parts) {
+  return parts > 1 ? (int64_t)parts * 2 * p.B * p.Hkv * p.N * p.d * (int64_t)sizeof(float) : 0;
+}
+
 // Built in fb_passes_d128.hip.
 extern template int32_t launch_pass1<bf16, 128>(const Problem&, const void*, const void*, const void*, const void*,
                                                 const void*, const void*, const void*, const void*, const float*,
                                                 const float*, const void*, void*, void*, float*, float*, hipStream_t);
 extern template int32_t launch_pass2<bf16, 128>(const Problem&, const void*, const void*, const void*, const void*,
                                                 const void*, const void*, const void*, const float*, const float*,
-                                                const float*, const float*, void*, void*, hipStream_t);
+                                                const float*, const float*, void*, void*, hipStream_t, float*,
+                                                int);
 
 }  // namespace fb

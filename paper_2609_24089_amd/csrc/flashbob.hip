@@ -39,6 +39,42 @@ bool use_two_sets(int workgroups) {
     return BOB_EUNSUPPORTED;                                                     \
   } while (0)
 
+// The mode of bob_set_column_split (0 automatic, 1 never, 2..8 that many
+// parts wherever the kernels run).
+static std::atomic<int> g_split{0};
+constexpr int kMaxParts = 8;
+
+// Automatic choice, from interleaved timing of Pass 2 at B1 H16 N16384
+// d128 bf16 with 1, 2, 4 and 16 key/value heads.  Causal: a column block's
+// work grows with the query tiles at or below its diagonal, and splitting
+// until there are about 8 jobs per CU made the heaviest block's share short
+// enough to balance (1.4-1.9x faster Pass 2 with 1-4 key/value heads; no gain
+// with 16).  Dense: blocks are equal, and the only gain was filling both
+// workgroup slots of each CU on a grid smaller than the CU count (6% with one
+// key/value head, against two wave sets in one workgroup).
+int column_parts(int workgroups, bool causal) {
+  const int mode = g_split.load(std::memory_order_relaxed);
+  if (mode >= 2) return mode;
+  if (mode == 1 || workgroups <= 0) return 1;
+  const int cus = device_cus();
+  if (cus <= 0 || (!causal && workgroups > cus)) return 1;
+  const int64_t target = (int64_t)(causal ? 8 : 2) * cus;
+  const int64_t parts = (target + workgroups - 1) / workgroups;
+  return parts < 2 ? 1 : (int)std::min<int64_t>(parts, kMaxParts);
+}
+
+// Parts of a validated, supported problem's Pass 2.
+static int pass2_parts_of(const Problem& p) {
+  if (p.dtype == BOB_BF16 && p.d == 32) return pass2_parts<bf16, 32>(p);
+  if (p.dtype == BOB_BF16 && p.d == 64) return pass2_parts<bf16, 64>(p);
+  if (p.dtype == BOB_BF16 && p.d == 128) return pass2_parts<bf16, 128>(p);
+  if (p.dtype == BOB_BF16 && p.d == 256) return pass2_parts<bf16, 256>(p);
+  if (p.dtype == BOB_F32 && p.d == 32) return pass2_parts<float, 32>(p);
+  if (p.dtype == BOB_F32 && p.d == 64) return pass2_parts<float, 64>(p);
+  if (p.dtype == BOB_F32 && p.d == 128) return pass2_parts<float, 128>(p);
+  return 1;
+}
+
 }  // namespace fb
 
 using fb::Problem;
@@ -156,6 +192,35 @@ int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
               (hipStream_t)stream);
 }
 
+int64_t bob_pass2_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                  int32_t causal) {
+  const Problem p{dtype, B, H, N, d, 1.0f, causal, Hkv};
+  bool empty;
+  if (fb::check_problem(p, &empty) != BOB_OK || empty) return 0;
+  return fb::pass2_workspace_bytes(p, fb::pass2_parts_of(p));
+}
+
+int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                   float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                   const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                   const float* L, const float* D, const float* alpha, const float* E, void* Kt,
+                                   void* Vt, void* workspace, int64_t workspace_bytes, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
+  if (rc != BOB_OK) return rc;
+  const int parts = fb::pass2_parts_of(p);
+  if (parts > 1) {
+    if (workspace == nullptr || workspace_bytes < fb::pass2_workspace_bytes(p, parts) ||
+        fb::check_ptrs({workspace}) != BOB_OK)
+      return BOB_EINVAL;
+  }
+  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
+              (hipStream_t)stream, (float*)workspace, parts);
+}
+
 int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
                              int32_t causal, const void* Q, const void* K, const void* gdQ, const void* gdK,
                              const float* L, float* alpha, void* stream) {
@@ -202,6 +267,12 @@ const char* bob_version(void) { return "flashbob-gfx950 0.1"; }
 int32_t bob_set_column_wave_sets(int32_t mode) {
   if (mode < 0 || mode > 2) return BOB_EINVAL;
   fb::g_wave_sets.store(mode, std::memory_order_relaxed);
+  return BOB_OK;
+}
+
+int32_t bob_set_column_split(int32_t parts) {
+  if (parts < 0 || parts > fb::kMaxParts) return BOB_EINVAL;
+  fb::g_split.store(parts, std::memory_order_relaxed);
   return BOB_OK;
 }
 

@@ -196,3 +196,44 @@ def test_column_wave_set_mode_is_validated(lib):
         assert lib.bob_set_column_wave_sets(ok) == fb.BOB_OK
     with pytest.raises(ValueError):
         fb.set_column_wave_sets(5)
+
+
+def call_ws(lib, ws=ALIGNED, nbytes=1 << 40, bad_index=None, dtype=fb.BOB_BF16, B=1, H=4, Hkv=1, N=1000, d=64,
+            causal=1):
+    ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(13)]
+    if bad_index is not None:
+        ptrs[bad_index] = ctypes.c_void_p(0)
+    return lib.attn_bob_pass2_cols_gqa_ws(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs,
+                                          ctypes.c_void_p(ws), nbytes, None)
+
+
+def test_column_split_mode_and_workspace(lib):
+    """bob_set_column_split validates its mode; in a forced mode the workspace
+    size is parts x {Kt, Vt} x B*Hkv*N*d fp32 values, and the split call
+    rejects a missing, misaligned or short workspace (and every bad tensor
+    pointer) before any launch."""
+    try:
+        for bad in (-1, 9, 100):
+            assert lib.bob_set_column_split(bad) == fb.BOB_EINVAL
+        assert lib.bob_set_column_split(4) == fb.BOB_OK
+        need = 4 * 2 * 1 * 1 * 1000 * 64 * 4
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == need
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_F32, 2, 4, 2, 100, 32, 0) == 4 * 2 * 2 * 2 * 100 * 32 * 4
+        # empty, invalid and unsupported problems need none (the call reports them)
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 0, 64, 1) == 0
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 3, 1000, 64, 1) == 0
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1) == 0
+        assert call_ws(lib, ws=0) == fb.BOB_EINVAL
+        assert call_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
+        assert call_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
+        for i in range(13):
+            assert call_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
+        assert call_ws(lib, H=4, Hkv=3) == fb.BOB_EINVAL
+        assert call_ws(lib, d=96) == fb.BOB_EUNSUPPORTED
+        assert call_ws(lib, N=0, ws=0) == fb.BOB_OK               # empty: nothing to do
+        assert lib.bob_set_column_split(1) == fb.BOB_OK
+        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == 0
+        with pytest.raises(ValueError):
+            fb.set_column_split(9)
+    finally:
+        lib.bob_set_column_split(0)

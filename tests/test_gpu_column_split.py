@@ -1,0 +1,129 @@
+"""GPU parity of Pass 2 with each key/value column block split over several
+workgroups (attn_bob_pass2_cols_gqa_ws, forced with bob_set_column_split):
+every split is checked against the float64 oracle on multi-head and grouped
+problems, dense and causal, including splits into more parts than a block
+has (query head, query tile) iterations, so that some parts stream nothing
+and store zeros; the row-owned outputs must not depend on the split, and Kt,
+Vt must agree with the unsplit kernels to the rounding of the fp32 sums."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.parity_util import TOL, nrel, say
+from workloads import NAMES, as_f64, make_gqa_inputs
+
+pytestmark = pytest.mark.gpu
+
+OUTS = ("O", "L", "D", "dQ", "dK", "dV", "alpha", "E", "Qt", "dOt", "Kt", "Vt")
+
+CASES = [
+    # B, H, Hkv, N, d, dtype, causal, seed
+    (1, 2, 2, 255, 64, "bf16", True, 170),
+    (1, 4, 1, 161, 128, "bf16", True, 171),    # multi-query, 6 tiles per head
+    (1, 4, 1, 161, 128, "bf16", False, 172),
+    (2, 6, 2, 200, 32, "bf16", True, 173),
+    (1, 2, 1, 20, 64, "bf16", True, 174),      # 1 tile per head, 2 iterations: parts 2.. stream nothing
+    (1, 2, 2, 130, 64, "f32", True, 175),
+    (1, 2, 1, 100, 128, "f32", False, 176),
+    (1, 2, 1, 96, 256, "bf16", True, 177),     # one-wave-per-SIMD shape
+]
+
+
+def case_id(c):
+    return f"B{c[0]}H{c[1]}kv{c[2]}N{c[3]}d{c[4]}{c[5]}{'causal' if c[6] else ''}"
+
+
+@pytest.fixture
+def fb():
+    import paper_2609_24089_amd as m
+    m.load_library()
+    yield m
+    m.set_column_split(0)
+
+
+@pytest.mark.parametrize("case", CASES, ids=case_id)
+def test_split_matches_oracle_and_unsplit(fb, case):
+    B, H, Hkv, N, d, dt, causal, seed = case
+    say(f"[column split] {case_id(case)}")
+    x = make_gqa_inputs(B, H, Hkv, N, d, dt, seed)
+    scale = 1.0 / np.sqrt(d)
+    ref = oracle.bob_gqa(*[as_f64(x[n]) for n in NAMES], scale, causal=causal)
+    xd = {k: v.cuda() for k, v in x.items()}
+    lib = fb.load_library()
+    code = fb.BOB_BF16 if dt == "bf16" else fb.BOB_F32
+    fb.set_column_split(1)
+    assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == 0
+    base = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
+    torch.cuda.synchronize()
+    for parts in (2, 3, 8):
+        fb.set_column_split(parts)
+        assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == parts * 2 * B * Hkv * N * d * 4
+        out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
+        torch.cuda.synchronize()
+        errs = {k: nrel(as_f64(out[k]), ref[k]) for k in OUTS}
+        say(f"   parts {parts} errs", {k: f"{v:.2e}" for k, v in errs.items()})
+        for k, e in errs.items():
+            assert e <= TOL[dt], (parts, k, e)
+        for k in OUTS:
+            if k not in ("Kt", "Vt"):
+                assert torch.equal(out[k], base[k]), (parts, k)
+        for k in ("Kt", "Vt"):
+            diff = nrel(as_f64(out[k]), as_f64(base[k]))
+            assert diff <= (1e-2 if dt == "bf16" else 1e-5), (parts, k, diff)
+
+
+def test_split_on_a_side_stream(fb):
+    """The binding's workspace is kept from reuse until the kernels on the
+    caller's stream are done; results on a non-current stream equal those on
+    the current one."""
+    x = make_gqa_inputs(1, 4, 1, 300, 128, "bf16", 178)
+    xd = {k: v.cuda() for k, v in x.items()}
+    Q, K, V, dO, UQ, UK, UV = (xd[n] for n in NAMES)
+    scale = 128 ** -0.5
+    O, L = fb.attn_fwd_lse(Q, K, V, scale, True)
+    dQ, dK, dV, D = fb.attn_bwd(Q, K, V, O, dO, L, scale, True)
+    Qt, dOt, al, E = fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, scale, True, dQ=dQ)
+    fb.set_column_split(4)
+    ref = fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for _ in range(3):
+        outs.append(fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True, stream=side))
+    side.synchronize()
+    for kt, vt in outs:
+        assert torch.equal(kt, ref[0]) and torch.equal(vt, ref[1])
+
+
+def test_automatic_choice(fb):
+    """Mode 0 splits a causal grid up to about 8 jobs per CU (at most 8
+    parts), a dense grid only when it has fewer workgroups than CUs, and
+    leaves the multi-head workloads alone; the automatic result equals the
+    forced one bit for bit."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    lib = fb.load_library()
+    fb.set_column_split(0)
+    N, d = 16384, 128
+    grid = lambda Hkv: Hkv * (N // 64)          # bf16 d = 128 Pass 2: 64 key rows per workgroup
+    expect = lambda g, causal: (min(8, -(-8 * cus // g)) if causal else
+                                (min(8, -(-2 * cus // g)) if g <= cus else 1))
+    for Hkv, causal in ((1, 1), (1, 0), (4, 1), (4, 0), (16, 1), (16, 0)):
+        parts = expect(grid(Hkv), causal)
+        parts = parts if parts >= 2 else 1
+        want = 0 if parts == 1 else parts * 2 * Hkv * N * d * 4
+        got = lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal)
+        say(f"[column split] auto Hkv={Hkv} causal={causal} CUs {cus}: {got} bytes (parts {parts})")
+        assert got == want, (Hkv, causal, got, want)
+    # a small causal problem: automatic equals the forced part count
+    B, H, Hkv, n = 1, 4, 1, 500
+    g = -(-n // 64)
+    parts = min(8, -(-8 * cus // g))
+    xd = {k: v.cuda() for k, v in make_gqa_inputs(B, H, Hkv, n, 128, "bf16", 179).items()}
+    auto = fb.bob(*[xd[k] for k in NAMES], 0.1, causal=True)
+    fb.set_column_split(parts)
+    forced = fb.bob(*[xd[k] for k in NAMES], 0.1, causal=True)
+    torch.cuda.synchronize()
+    for k in OUTS:
+        assert torch.equal(auto[k], forced[k]), k

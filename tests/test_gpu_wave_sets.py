@@ -42,8 +42,10 @@ def case_id(c):
 def fb():
     import paper_2609_24089_amd as m
     m.load_library()
+    m.set_column_split(1)   # Pass 2 would otherwise split these small grids over workgroups
     yield m
     m.set_column_wave_sets(0)
+    m.set_column_split(0)
 
 
 def run(fb, xd, scale, causal, mode):
