@@ -32,8 +32,8 @@
  *          same value.
  *  pointers  device pointers owned by the caller, 16-byte aligned, on the
  *          current HIP device (the kernels run there).  The library
- *          allocates no memory (attn_bob_pass2_cols_gqa_ws takes its
- *          workspace from the caller); its only state is the modes set by
+ *          allocates no memory (the *_ws calls take their workspace from
+ *          the caller); its only state is the modes set by
  *          bob_set_column_wave_sets and bob_set_column_split and a
  *          per-device count of compute units.
  *          Outputs must not alias inputs.
@@ -166,6 +166,21 @@ int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t 
                                    const float* L, const float* D, const float* alpha, const float* E, void* Kt,
                                    void* Vt, void* workspace, int64_t workspace_bytes, void* stream);
 
+/* The first backward with its column kernel (dK, dV) split the same way:
+ * arguments as attn_bwd_gqa plus workspace and workspace_bytes, with the
+ * rules of attn_bob_pass2_cols_gqa_ws (its size from
+ * bob_bwd_workspace_bytes).  dQ and D do not depend on the split. */
+int32_t attn_bwd_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                        int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                        const float* L, void* dQ, void* dK, void* dV, float* D, void* workspace,
+                        int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes attn_bwd_gqa_ws needs, as bob_pass2_workspace_bytes (the
+ * first backward's column workgroups own their own number of key rows, so
+ * the part count can differ from Pass 2's). */
+int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                int32_t causal);
+
 /* Workspace bytes attn_bob_pass2_cols_gqa_ws needs for this problem on the
  * current device under the current bob_set_column_split mode: 0 when it
  * would not split (and for an empty or invalid problem, which that call
@@ -221,11 +236,11 @@ const char* bob_version(void);
  * BOB_EINVAL for a mode outside 0..2. */
 int32_t bob_set_column_wave_sets(int32_t mode);
 
-/* How many workgroups attn_bob_pass2_cols_gqa_ws gives each column block.
- * 0 (default): automatic, from the column grid, the device's compute units
- * and the mask; 1: never split; 2..8: always that many parts.  Process-wide
- * (all devices); read by bob_pass2_workspace_bytes and by the call itself,
- * which must see the same mode.  Returns BOB_OK, or BOB_EINVAL for a value
+/* How many workgroups attn_bwd_gqa_ws and attn_bob_pass2_cols_gqa_ws give
+ * each column block.  0 (default): automatic, from the column grid, the
+ * device's compute units and the mask; 1: never split; 2..8: always that
+ * many parts.  Process-wide (all devices); read by the *_workspace_bytes
+ * queries and by the calls themselves, which must see the same mode.  Returns BOB_OK, or BOB_EINVAL for a value
  * outside 0..8. */
 int32_t bob_set_column_split(int32_t parts);
 

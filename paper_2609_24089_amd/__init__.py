@@ -63,6 +63,10 @@ def load_library():
     lib.bob_pass2_workspace_bytes.restype = i64
     lib.attn_bob_pass2_cols_gqa_ws.argtypes = common_gqa + [vp] * 13 + [vp, i64] + [vp]
     lib.attn_bob_pass2_cols_gqa_ws.restype = i32
+    lib.bob_bwd_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32]
+    lib.bob_bwd_workspace_bytes.restype = i64
+    lib.attn_bwd_gqa_ws.argtypes = common_gqa + [vp] * 10 + [vp, i64] + [vp]
+    lib.attn_bwd_gqa_ws.restype = i32
     _lib = lib
     return lib
 
@@ -80,8 +84,9 @@ def set_column_wave_sets(mode):
 
 
 def set_column_split(parts):
-    """bob_set_column_split: 0 automatic (default), 1 never split a Pass 2
-    column block over workgroups, 2..8 always split it into that many."""
+    """bob_set_column_split: 0 automatic (default), 1 never split a column
+    block of the first backward or Pass 2 over workgroups, 2..8 always split
+    it into that many."""
     rc = load_library().bob_set_column_split(int(parts))
     if rc != BOB_OK:
         raise ValueError(f"bob_set_column_split({parts}): {status_string(rc)}")
@@ -155,6 +160,21 @@ def _call(like, fn, *args):
         raise RuntimeError(status_string(rc))
 
 
+def _column_workspace(query, code, B, H, Hkv, N, d, causal, like, stream):
+    """(workspace, bytes) for a *_ws call whose column blocks the library
+    would split over workgroups (query: its bob_*_workspace_bytes), else
+    (None, 0).  The fp32 partial sums go to a buffer from torch's allocator,
+    kept from reuse until the kernels on `stream` are done."""
+    with torch.cuda.device(like.device):
+        nbytes = query(code, B, H, Hkv, N, d, causal)
+    if nbytes <= 0:
+        return None, 0
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
+    if stream is not None:
+        ws.record_stream(stream)
+    return ws, nbytes
+
+
 def _rows_empty(shape, like):
     return torch.empty(tuple(shape[:3]), dtype=torch.float32, device=like.device)
 
@@ -188,11 +208,16 @@ def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
     _check_mats(K, dK, dV)
     _check_rows(Q.shape, D)
     lib = load_library()
-    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D), _stream(stream, Q))
-    if Hkv == H:
-        _call(Q, lib.attn_bwd, _dtype_code(Q), B, H, N, d, float(scale), int(bool(causal)), *ptrs)
+    code, c = _dtype_code(Q), int(bool(causal))
+    ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D))
+    st = _stream(stream, Q)
+    ws, nbytes = _column_workspace(lib.bob_bwd_workspace_bytes, code, B, H, Hkv, N, d, c, Q, stream)
+    if ws is not None:
+        _call(Q, lib.attn_bwd_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _p(ws), nbytes, st)
+    elif Hkv == H:
+        _call(Q, lib.attn_bwd, code, B, H, N, d, float(scale), c, *ptrs, st)
     else:
-        _call(Q, lib.attn_bwd_gqa, _dtype_code(Q), B, H, Hkv, N, d, float(scale), int(bool(causal)), *ptrs)
+        _call(Q, lib.attn_bwd_gqa, code, B, H, Hkv, N, d, float(scale), c, *ptrs, st)
     return dQ, dK, dV, D
 
 
@@ -235,15 +260,8 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
     ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
             _p(Kt), _p(Vt))
     st = _stream(stream, Q)
-    with torch.cuda.device(Q.device):
-        nbytes = lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, c)
-    if nbytes > 0:
-        # column blocks split over workgroups: fp32 partial sums in a
-        # workspace from torch's allocator, kept from reuse until the
-        # kernels on `stream` are done
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=Q.device)
-        if stream is not None:
-            ws.record_stream(stream)
+    ws, nbytes = _column_workspace(lib.bob_pass2_workspace_bytes, code, B, H, Hkv, N, d, c, Q, stream)
+    if ws is not None:
         _call(Q, lib.attn_bob_pass2_cols_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _p(ws), nbytes,
               st)
     elif Hkv == H:

@@ -496,6 +496,46 @@ struct StreamSplit {
   }
 };
 
+// Job numbering of a column kernel whose column blocks are split over
+// nparts workgroups (grid = total * nparts, total = heads * nRB):
+// job = (rb * heads + bh) * nparts + part.  Under the causal mask block rb
+// holds work in proportion to the tiles at or below its diagonal, so jobs run
+// heaviest first, and consecutive jobs (which the dispatcher sends to
+// different XCDs) carry similar work.
+__device__ __forceinline__ void map_column_job(int nRB, int total, int nparts, int& bh, int& rb, int& part) {
+  const int heads = total / nRB, job = blockIdx.x;
+  rb = job / (heads * nparts);
+  const int rest = job - rb * heads * nparts;
+  bh = rest / nparts;
+  part = rest - bh * nparts;
+}
+
+// One part's fp32 sums of a split column kernel: x and y (the two key-side
+// accumulators, [16-dim block][stationary sub-block]) of the lane's rows
+// col0 + 16 m + (lane & 15) go to planes 2 part and 2 part + 1 of parts_out
+// ([nparts][2][heads][N][D]), at head offset hoff.  Every part stores all
+// of its rows, zeros included, so the reduction needs no cleared buffer.
+template <int D, int NB, int MC>
+__device__ __forceinline__ void store_column_part(float* parts_out, int64_t plane, int part, int64_t hoff,
+                                                  int col0, int N, const floatx4 (&x)[NB][MC],
+                                                  const floatx4 (&y)[NB][MC]) {
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  float* px = parts_out + 2 * (int64_t)part * plane;
+  float* py = px + plane;
+#pragma unroll
+  for (int mc = 0; mc < MC; ++mc) {
+    const int col = col0 + 16 * mc + j;
+    if (col < N) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int64_t off = hoff + (int64_t)col * D + 16 * nb + 4 * g;
+        *(floatx4*)(px + off) = x[nb][mc];
+        *(floatx4*)(py + off) = y[nb][mc];
+      }
+    }
+  }
+}
+
 // Two wave sets of one workgroup that accumulated the same stationary rows
 // over disjoint sets of streamed tiles: set 1 hands its fp32 accumulators x,
 // then y, to set 0 through LDS (buf: every wave's A*B 1 KB blocks, placed by

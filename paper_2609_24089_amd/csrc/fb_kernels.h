@@ -279,11 +279,12 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // are added through LDS at the end (KS = 2 fills a CU when the grid has no
 // more workgroups than CUs).
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kParts = false>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
-    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal, int grp) {
+    T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal, int grp,
+    float* __restrict__ parts_out = nullptr, int nparts = 1) {
   static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
@@ -301,8 +302,11 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   auto& rawsc = sm.rawsc;
   auto& tsc = sm.tsc;
 
-  int bh, rb;
-  map_block(nRB, total, bh, rb);
+  int bh, rb, part = 0;
+  if constexpr (kParts)
+    map_column_job(nRB, total, nparts, bh, rb, part);
+  else
+    map_block(nRB, total, bh, rb);
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int ks = KS == 1 ? 0 : wave_id() / NW;       // wave set
@@ -342,7 +346,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   const int nT = (N + kBS - 1) / kBS;
   const int it_begin = causal ? (rb * BC) / kBS : 0;
   const int nTh = nT - it_begin;
-  const StreamSplit<kGQA, KS> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp};
+  const StreamSplit<kGQA, KS, kParts> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp, part, nparts};
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 2>(), 1>(
       sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
@@ -421,6 +425,10 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     static_assert(sizeof(lds) >= (size_t)NW * G::kNB * MC * 1024, "set merge buffer");
     merge_wave_sets(dk, dv, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);
     if (ks != 0) return;
+  }
+  if constexpr (kParts) {
+    store_column_part<D>(parts_out, (int64_t)(total / nRB) * N * D, part, hoff, col0, N, dk, dv);
+    return;
   }
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
@@ -791,7 +799,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 // the first backward.  With kParts each column block is split over nparts
 // workgroups, which store fp32 partial sums of Kt / tau and Vt / tau to
 // parts_out ([nparts][2][B*Hkv][N][d]; bob_column_parts_reduce_kernel adds
-// them); the grid then holds total * nparts jobs, heaviest column block first.
+// them); the grid then holds total * nparts jobs (map_column_job).
 // ===========================================================================
 template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kPF,
           bool kParts = false>
@@ -824,19 +832,10 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   auto& tsc = sm.tsc;
 
   int bh, rb, part = 0;
-  if constexpr (kParts) {
-    // job = (rb * heads + bh) * nparts + part: under the causal mask block rb
-    // holds work in proportion to the tiles at or below its diagonal, so the
-    // jobs run heaviest first, and consecutive jobs (which go to different
-    // XCDs) carry similar work
-    const int heads = total / nRB, job = blockIdx.x;
-    rb = job / (heads * nparts);
-    const int rest = job - rb * heads * nparts;
-    bh = rest / nparts;
-    part = rest - bh * nparts;
-  } else {
+  if constexpr (kParts)
+    map_column_job(nRB, total, nparts, bh, rb, part);
+  else
     map_block(nRB, total, bh, rb);
-  }
   const int64_t hoff = (int64_t)bh * N * D;
   const int l = lane_id(), g = l >> 4, j = l & 15;
   const int ks = KS == 1 ? 0 : wave_id() / NW;       // wave set
@@ -1029,23 +1028,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     if (ks != 0) return;
   }
   if constexpr (kParts) {
-    // every part stores all of its rows, zeros included, so the reduction
-    // needs no cleared buffer
-    const int64_t plane = (int64_t)(total / nRB) * N * D;
-    float* pk = parts_out + 2 * (int64_t)part * plane;
-    float* pv = pk + plane;
-#pragma unroll
-    for (int mc = 0; mc < MC; ++mc) {
-      const int col = col0 + 16 * mc + j;
-      if (col < N) {
-#pragma unroll
-        for (int nb = 0; nb < G::kNB; ++nb) {
-          const int64_t off = hoff + (int64_t)col * D + 16 * nb + 4 * g;
-          *(floatx4*)(pk + off) = aK[nb][mc];
-          *(floatx4*)(pv + off) = aV[nb][mc];
-        }
-      }
-    }
+    store_column_part<D>(parts_out, (int64_t)(total / nRB) * N * D, part, hoff, col0, N, aK, aV);
     return;
   }
 #pragma unroll
@@ -1062,12 +1045,15 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   }
 }
 
-// Sum of the nparts fp32 partial Kt / tau and Vt / tau planes of a split
-// Pass 2 (plane elements each, laid out [nparts][2][plane]), in part order,
-// times scale, rounded to the output type.  plane is a multiple of 4.
+// Sum of the nparts fp32 partial planes of a split column kernel (plane
+// elements each, laid out [nparts][2][plane]), in part order, times scale_k
+// (first plane of each part, into Kt) or scale_v (second, into Vt), rounded
+// to the output type.  Pass 2 stores Kt / tau and Vt / tau (both scales
+// tau); the first backward stores dK / tau and dV (scales tau and 1).
+// plane is a multiple of 4.
 template <typename T>
 __global__ __launch_bounds__(256) void bob_column_parts_reduce_kernel(const float* __restrict__ parts, int nparts,
-                                                                      int64_t plane, float scale,
+                                                                      int64_t plane, float scale_k, float scale_v,
                                                                       T* __restrict__ Kt, T* __restrict__ Vt) {
   using E = Elt<T>;
   const int64_t n4 = plane / 4;
@@ -1076,7 +1062,7 @@ __global__ __launch_bounds__(256) void bob_column_parts_reduce_kernel(const floa
     const int64_t off = 4 * (i - t * n4);
     floatx4 acc = *(const floatx4*)(parts + t * plane + off);
     for (int q = 1; q < nparts; ++q) acc += *(const floatx4*)(parts + (2 * (int64_t)q + t) * plane + off);
-    E::store4((t == 0 ? Kt : Vt) + off, acc * scale);
+    E::store4((t == 0 ? Kt : Vt) + off, acc * (t == 0 ? scale_k : scale_v));
   }
 }
 

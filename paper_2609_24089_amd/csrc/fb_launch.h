@@ -165,7 +165,7 @@ int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V
 template <typename T, int D>
 int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
                    const void* dO, const float* L, void* dQ, void* dK, void* dV, float* Dv,
-                   hipStream_t s) {
+                   hipStream_t s, float* parts_ws = nullptr, int parts = 1) {
   constexpr Shape cr = Cfg<T, D>::kRows, cc = Cfg<T, D>::kCols;
   const Grid gr = grid_for(p, 16 * cr.mr * cr.nw);
   (void)hipGetLastError();
@@ -177,6 +177,18 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
   const Grid gc = grid_for(p, 16 * cc.mr * cc.nw, true);
   const bool two = use_two_sets(gc.total);
   (void)hipGetLastError();
+  if (parts > 1) {
+    // each column block split over `parts` workgroups, then one reduction
+    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true, 1, true>),
+                       dim3(gc.total * parts), dim3(64 * cc.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
+                       (const T*)dO, L, (const float*)Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
+                       p.causal, group(p), parts_ws, parts);
+    const int64_t plane = p.B * p.Hkv * p.N * p.d;
+    const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
+    hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
+                       parts, plane, p.scale, 1.0f, (T*)dK, (T*)dV);
+    return finish_launch();
+  }
   auto cols = [&](auto gqa, auto ks) {
     hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, decltype(gqa)::value, decltype(ks)::value>),
                        dim3(gc.total), dim3(64 * cc.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V,
@@ -264,7 +276,7 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
     const int64_t plane = p.B * p.Hkv * p.N * p.d;
     const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
     hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
-                       parts, plane, p.scale, (T*)Kt, (T*)Vt);
+                       parts, plane, p.scale, p.scale, (T*)Kt, (T*)Vt);
     return finish_launch();
   }
   const bool two = use_two_sets(g.total);
@@ -285,20 +297,30 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
   return finish_launch();
 }
 
-// How many workgroups share a Pass 2 column block (1: no split), from the
-// mode set by bob_set_column_split, the column grid and the mask.
-int column_parts(int workgroups, bool causal);
+// How many workgroups share a column block of the first backward's or Pass
+// 2's column kernel (1: no split), from the mode set by
+// bob_set_column_split, the kernel's column grid and the mask.
+int column_parts(int workgroups, bool causal, bool pass2);
+
+template <typename T, int D>
+int bwd_parts(const Problem& p) {
+  constexpr Shape c = Cfg<T, D>::kCols;
+  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
+  const int parts = column_parts(g.total, p.causal != 0, false);
+  return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
+}
 
 template <typename T, int D>
 int pass2_parts(const Problem& p) {
   constexpr Shape c = Cfg<T, D>::kP2;
   const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const int parts = column_parts(g.total, p.causal != 0);
+  const int parts = column_parts(g.total, p.causal != 0, true);
   return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
 }
 
-// fp32 workspace of a split Pass 2: parts x {Kt, Vt} x B*Hkv*N*d.
-inline int64_t pass2_workspace_bytes(const Problem& p, int parts) {
+// fp32 workspace of a split column kernel: parts x {Kt, Vt} (or {dK, dV})
+// x B*Hkv*N*d.
+inline int64_t column_workspace_bytes(const Problem& p, int parts) {
   return parts > 1 ? (int64_t)parts * 2 * p.B * p.Hkv * p.N * p.d * (int64_t)sizeof(float) : 0;
 }
 

@@ -1,5 +1,7 @@
 // C ABI of libflashbob.so: argument validation and kernel dispatch.
 // The entry points are declared (and documented) in include/flashbob.h.
+#include <type_traits>
+
 #include "fb_launch.h"
 
 namespace fb {
@@ -44,35 +46,58 @@ bool use_two_sets(int workgroups) {
 static std::atomic<int> g_split{0};
 constexpr int kMaxParts = 8;
 
-// Automatic choice, from interleaved timing of Pass 2 at B1 H16 N16384
-// d128 bf16 with 1, 2, 4 and 16 key/value heads.  Causal: a column block's
-// work grows with the query tiles at or below its diagonal, and splitting
-// until there are about 8 jobs per CU made the heaviest block's share short
-// enough to balance (1.4-1.9x faster Pass 2 with 1-4 key/value heads; no gain
-// with 16).  Dense: blocks are equal, and the only gain was filling both
-// workgroup slots of each CU on a grid smaller than the CU count (6% with one
-// key/value head, against two wave sets in one workgroup).
-int column_parts(int workgroups, bool causal) {
+// Automatic choice, from interleaved timing at B1 H16 N16384 d128 bf16 with
+// 1, 2, 4 and 16 key/value heads.  Causal: a column block's work grows with
+// the query tiles at or below its diagonal, and splitting until there are
+// about 8 jobs per CU made the heaviest block's share short enough to
+// balance (Pass 2 and the first backward 1.3-2x faster with 1-4 key/value
+// heads; no gain with 16).  Dense Pass 2: blocks are equal, and the only gain
+// was filling both workgroup slots of each CU on a grid smaller than the CU
+// count (6% with one key/value head, against two wave sets in one
+// workgroup).  The dense first backward gained from the same 8 jobs per CU
+// as the causal one (9-18% with 1 and 4 key/value heads).
+int column_parts(int workgroups, bool causal, bool pass2) {
   const int mode = g_split.load(std::memory_order_relaxed);
   if (mode >= 2) return mode;
   if (mode == 1 || workgroups <= 0) return 1;
   const int cus = device_cus();
-  if (cus <= 0 || (!causal && workgroups > cus)) return 1;
-  const int64_t target = (int64_t)(causal ? 8 : 2) * cus;
+  const bool fill_only = pass2 && !causal;
+  if (cus <= 0 || (fill_only && workgroups > cus)) return 1;
+  const int64_t target = (int64_t)(fill_only ? 2 : 8) * cus;
   const int64_t parts = (target + workgroups - 1) / workgroups;
   return parts < 2 ? 1 : (int)std::min<int64_t>(parts, kMaxParts);
 }
 
-// Parts of a validated, supported problem's Pass 2.
-static int pass2_parts_of(const Problem& p) {
-  if (p.dtype == BOB_BF16 && p.d == 32) return pass2_parts<bf16, 32>(p);
-  if (p.dtype == BOB_BF16 && p.d == 64) return pass2_parts<bf16, 64>(p);
-  if (p.dtype == BOB_BF16 && p.d == 128) return pass2_parts<bf16, 128>(p);
-  if (p.dtype == BOB_BF16 && p.d == 256) return pass2_parts<bf16, 256>(p);
-  if (p.dtype == BOB_F32 && p.d == 32) return pass2_parts<float, 32>(p);
-  if (p.dtype == BOB_F32 && p.d == 64) return pass2_parts<float, 64>(p);
-  if (p.dtype == BOB_F32 && p.d == 128) return pass2_parts<float, 128>(p);
+// Parts of a validated, supported problem's column kernel: Pass 2's
+// (pass2 = true) or the first backward's.
+static int column_parts_of(const Problem& p, bool pass2) {
+#define FB_PARTS(TT, DD) \
+  if (p.dtype == (std::is_same<TT, float>::value ? BOB_F32 : BOB_BF16) && p.d == DD) \
+    return pass2 ? pass2_parts<TT, DD>(p) : bwd_parts<TT, DD>(p);
+  FB_PARTS(bf16, 32)
+  FB_PARTS(bf16, 64)
+  FB_PARTS(bf16, 128)
+  FB_PARTS(bf16, 256)
+  FB_PARTS(float, 32)
+  FB_PARTS(float, 64)
+  FB_PARTS(float, 128)
+#undef FB_PARTS
   return 1;
+}
+
+// Workspace of a column kernel's split for the *_ws entry points (0 when
+// it would not split, or for an empty or invalid problem).
+static int64_t column_ws_bytes(const Problem& p, bool pass2) {
+  bool empty;
+  if (check_problem(p, &empty) != BOB_OK || empty) return 0;
+  return column_workspace_bytes(p, column_parts_of(p, pass2));
+}
+
+// The workspace checks of a *_ws entry point for a valid, non-empty problem
+// that splits into `parts` (> 1).
+static int32_t check_workspace(const Problem& p, int parts, const void* ws, int64_t bytes) {
+  if (ws == nullptr || bytes < column_workspace_bytes(p, parts) || check_ptrs({ws}) != BOB_OK) return BOB_EINVAL;
+  return BOB_OK;
 }
 
 }  // namespace fb
@@ -194,10 +219,28 @@ int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
 
 int64_t bob_pass2_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
                                   int32_t causal) {
-  const Problem p{dtype, B, H, N, d, 1.0f, causal, Hkv};
+  return fb::column_ws_bytes(Problem{dtype, B, H, N, d, 1.0f, causal, Hkv}, true);
+}
+
+int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                int32_t causal) {
+  return fb::column_ws_bytes(Problem{dtype, B, H, N, d, 1.0f, causal, Hkv}, false);
+}
+
+int32_t attn_bwd_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
+                        int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                        const float* L, void* dQ, void* dK, void* dV, float* D, void* workspace,
+                        int64_t workspace_bytes, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
   bool empty;
-  if (fb::check_problem(p, &empty) != BOB_OK || empty) return 0;
-  return fb::pass2_workspace_bytes(p, fb::pass2_parts_of(p));
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK || empty) return rc;
+  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
+  if (rc != BOB_OK) return rc;
+  const int parts = fb::column_parts_of(p, false);
+  if (parts > 1 && (rc = fb::check_workspace(p, parts, workspace, workspace_bytes)) != BOB_OK) return rc;
+  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream, (float*)workspace,
+              parts);
 }
 
 int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
@@ -211,12 +254,8 @@ int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t 
   if (rc != BOB_OK || empty) return rc;
   rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
   if (rc != BOB_OK) return rc;
-  const int parts = fb::pass2_parts_of(p);
-  if (parts > 1) {
-    if (workspace == nullptr || workspace_bytes < fb::pass2_workspace_bytes(p, parts) ||
-        fb::check_ptrs({workspace}) != BOB_OK)
-      return BOB_EINVAL;
-  }
+  const int parts = fb::column_parts_of(p, true);
+  if (parts > 1 && (rc = fb::check_workspace(p, parts, workspace, workspace_bytes)) != BOB_OK) return rc;
   FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
               (hipStream_t)stream, (float*)workspace, parts);
 }

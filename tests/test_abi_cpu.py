@@ -207,6 +207,15 @@ def call_ws(lib, ws=ALIGNED, nbytes=1 << 40, bad_index=None, dtype=fb.BOB_BF16, 
                                           ctypes.c_void_p(ws), nbytes, None)
 
 
+def call_bwd_ws(lib, ws=ALIGNED, nbytes=1 << 40, bad_index=None, dtype=fb.BOB_BF16, B=1, H=4, Hkv=1, N=1000,
+                d=64, causal=1):
+    ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(10)]
+    if bad_index is not None:
+        ptrs[bad_index] = ctypes.c_void_p(0)
+    return lib.attn_bwd_gqa_ws(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs, ctypes.c_void_p(ws),
+                               nbytes, None)
+
+
 def test_column_split_mode_and_workspace(lib):
     """bob_set_column_split validates its mode; in a forced mode the workspace
     size is parts x {Kt, Vt} x B*Hkv*N*d fp32 values, and the split call
@@ -231,8 +240,18 @@ def test_column_split_mode_and_workspace(lib):
         assert call_ws(lib, H=4, Hkv=3) == fb.BOB_EINVAL
         assert call_ws(lib, d=96) == fb.BOB_EUNSUPPORTED
         assert call_ws(lib, N=0, ws=0) == fb.BOB_OK               # empty: nothing to do
+        # the first backward's split: same size rule and the same checks
+        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == need
+        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1) == 0
+        assert call_bwd_ws(lib, ws=0) == fb.BOB_EINVAL
+        assert call_bwd_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
+        assert call_bwd_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
+        for i in range(10):
+            assert call_bwd_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
+        assert call_bwd_ws(lib, N=0, ws=0) == fb.BOB_OK
         assert lib.bob_set_column_split(1) == fb.BOB_OK
         assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == 0
+        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == 0
         with pytest.raises(ValueError):
             fb.set_column_split(9)
     finally:

@@ -1,10 +1,13 @@
-"""GPU parity of Pass 2 with each key/value column block split over several
-workgroups (attn_bob_pass2_cols_gqa_ws, forced with bob_set_column_split):
+"""GPU parity of the column kernels (the first backward's dK, dV and Pass
+2's Kt, Vt) with each key/value column block split over several workgroups
+(attn_bwd_gqa_ws, attn_bob_pass2_cols_gqa_ws; forced with
+bob_set_column_split):
 every split is checked against the float64 oracle on multi-head and grouped
 problems, dense and causal, including splits into more parts than a block
 has (query head, query tile) iterations, so that some parts stream nothing
-and store zeros; the row-owned outputs must not depend on the split, and Kt,
-Vt must agree with the unsplit kernels to the rounding of the fp32 sums."""
+and store zeros; the row-owned outputs must not depend on the split, and dK,
+dV, Kt, Vt must agree with the unsplit kernels to the rounding of the fp32
+sums."""
 import numpy as np
 import pytest
 import torch
@@ -16,6 +19,7 @@ from workloads import NAMES, as_f64, make_gqa_inputs
 pytestmark = pytest.mark.gpu
 
 OUTS = ("O", "L", "D", "dQ", "dK", "dV", "alpha", "E", "Qt", "dOt", "Kt", "Vt")
+COLUMN_OUTS = ("dK", "dV", "Kt", "Vt")
 
 CASES = [
     # B, H, Hkv, N, d, dtype, causal, seed
@@ -54,11 +58,14 @@ def test_split_matches_oracle_and_unsplit(fb, case):
     code = fb.BOB_BF16 if dt == "bf16" else fb.BOB_F32
     fb.set_column_split(1)
     assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == 0
+    assert lib.bob_bwd_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == 0
     base = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
     torch.cuda.synchronize()
     for parts in (2, 3, 8):
         fb.set_column_split(parts)
-        assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == parts * 2 * B * Hkv * N * d * 4
+        want = parts * 2 * B * Hkv * N * d * 4
+        assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == want
+        assert lib.bob_bwd_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == want
         out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
         torch.cuda.synchronize()
         errs = {k: nrel(as_f64(out[k]), ref[k]) for k in OUTS}
@@ -66,9 +73,9 @@ def test_split_matches_oracle_and_unsplit(fb, case):
         for k, e in errs.items():
             assert e <= TOL[dt], (parts, k, e)
         for k in OUTS:
-            if k not in ("Kt", "Vt"):
+            if k not in COLUMN_OUTS:
                 assert torch.equal(out[k], base[k]), (parts, k)
-        for k in ("Kt", "Vt"):
+        for k in COLUMN_OUTS:
             diff = nrel(as_f64(out[k]), as_f64(base[k]))
             assert diff <= (1e-2 if dt == "bf16" else 1e-5), (parts, k, diff)
 
@@ -99,9 +106,10 @@ def test_split_on_a_side_stream(fb):
 
 def test_automatic_choice(fb):
     """Mode 0 splits a causal grid up to about 8 jobs per CU (at most 8
-    parts), a dense grid only when it has fewer workgroups than CUs, and
-    leaves the multi-head workloads alone; the automatic result equals the
-    forced one bit for bit."""
+    parts); Pass 2 splits a dense grid only when it has fewer workgroups than
+    CUs, the first backward to about 8 jobs per CU as well; the multi-head
+    workloads stay unsplit; the automatic result equals the forced one bit
+    for bit."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     lib = fb.load_library()
     fb.set_column_split(0)
@@ -116,6 +124,11 @@ def test_automatic_choice(fb):
         got = lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal)
         say(f"[column split] auto Hkv={Hkv} causal={causal} CUs {cus}: {got} bytes (parts {parts})")
         assert got == want, (Hkv, causal, got, want)
+        # the first backward's column kernel also owns 64 key rows per
+        # workgroup here, and is split to about 8 jobs per CU under either mask
+        pb = min(8, -(-8 * cus // grid(Hkv)))
+        want_b = 0 if pb < 2 else pb * 2 * Hkv * N * d * 4
+        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal) == want_b, (Hkv, causal)
     # a small causal problem: automatic equals the forced part count
     B, H, Hkv, n = 1, 4, 1, 500
     g = -(-n // 64)
