@@ -21,7 +21,10 @@
 // stream the grp query heads of that key/value head one after another, so
 // their key-side outputs sum over the group with no atomics.  On grids with
 // no more workgroups than CUs a column workgroup holds two wave sets that
-// split those streamed tiles and add their partial sums through LDS.
+// split those streamed tiles and add their partial sums through LDS.  The
+// kParts forms split a column block over several workgroups instead, each
+// storing fp32 partial sums to a caller's workspace that
+// bob_column_parts_reduce_kernel adds (small or causal grids).
 #pragma once
 #include "fb_common.h"
 
