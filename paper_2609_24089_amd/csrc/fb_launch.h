@@ -300,13 +300,17 @@ int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void*
 // How many workgroups share a column block of the first backward's or Pass
 // 2's column kernel (1: no split), from the mode set by
 // bob_set_column_split, the kernel's column grid and the mask.
-int column_parts(int workgroups, bool causal, bool pass2);
+int column_parts(int workgroups, bool causal, bool pass2, int64_t iters_per_block);
+
+// Streamed iterations of one column block: its group's query heads times
+// 32-row query tiles (fewer under the causal mask).
+inline int64_t column_iters(const Problem& p) { return (int64_t)group(p) * ((p.N + 31) / 32); }
 
 template <typename T, int D>
 int bwd_parts(const Problem& p) {
   constexpr Shape c = Cfg<T, D>::kCols;
   const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const int parts = column_parts(g.total, p.causal != 0, false);
+  const int parts = column_parts(g.total, p.causal != 0, false, column_iters(p));
   return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
 }
 
@@ -314,7 +318,7 @@ template <typename T, int D>
 int pass2_parts(const Problem& p) {
   constexpr Shape c = Cfg<T, D>::kP2;
   const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const int parts = column_parts(g.total, p.causal != 0, true);
+  const int parts = column_parts(g.total, p.causal != 0, true, column_iters(p));
   return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
 }
 

@@ -55,11 +55,16 @@ constexpr int kMaxParts = 8;
 // was filling both workgroup slots of each CU on a grid smaller than the CU
 // count (6% with one key/value head, against two wave sets in one
 // workgroup).  The dense first backward gained from the same 8 jobs per CU
-// as the causal one (9-18% with 1 and 4 key/value heads).
-int column_parts(int workgroups, bool causal, bool pass2) {
+// as the causal one (9-18% with 1 and 4 key/value heads).  Either kernel
+// only splits blocks of at least 1024 streamed iterations (query heads per
+// group x 32-row query tiles): on the causal B4 H12 problems at N = 2048 and
+// 4096 (64 and 128 iterations), the parts' fp32 round trip through HBM cost
+// more than the balance gained (up to 14% slower), while every gain above
+// came from blocks of 2048 iterations or more.
+int column_parts(int workgroups, bool causal, bool pass2, int64_t iters_per_block) {
   const int mode = g_split.load(std::memory_order_relaxed);
   if (mode >= 2) return mode;
-  if (mode == 1 || workgroups <= 0) return 1;
+  if (mode == 1 || workgroups <= 0 || iters_per_block < 1024) return 1;
   const int cus = device_cus();
   const bool fill_only = pass2 && !causal;
   if (cus <= 0 || (fill_only && workgroups > cus)) return 1;

@@ -107,9 +107,9 @@ def test_split_on_a_side_stream(fb):
 def test_automatic_choice(fb):
     """Mode 0 splits a causal grid up to about 8 jobs per CU (at most 8
     parts); Pass 2 splits a dense grid only when it has fewer workgroups than
-    CUs, the first backward to about 8 jobs per CU as well; the multi-head
-    workloads stay unsplit; the automatic result equals the forced one bit
-    for bit."""
+    CUs, the first backward to about 8 jobs per CU as well; blocks of fewer
+    than 1024 streamed iterations and the multi-head workloads stay
+    unsplit; the automatic result equals the forced one bit for bit."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     lib = fb.load_library()
     fb.set_column_split(0)
@@ -129,8 +129,14 @@ def test_automatic_choice(fb):
         pb = min(8, -(-8 * cus // grid(Hkv)))
         want_b = 0 if pb < 2 else pb * 2 * Hkv * N * d * 4
         assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal) == want_b, (Hkv, causal)
-    # a small causal problem: automatic equals the forced part count
-    B, H, Hkv, n = 1, 4, 1, 500
+    # short blocks (fewer than 1024 streamed iterations) are never split
+    for Hkv, n in ((12, 4096), (12, 2048), (1, 500)):
+        for causal in (0, 1):
+            assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
+            assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
+    # a causal multi-query problem with 16 x 64 = 1024 iterations per block:
+    # automatic equals the forced part count
+    B, H, Hkv, n = 1, 16, 1, 2048
     g = -(-n // 64)
     parts = min(8, -(-8 * cus // g))
     xd = {k: v.cuda() for k, v in make_gqa_inputs(B, H, Hkv, n, 128, "bf16", 179).items()}
