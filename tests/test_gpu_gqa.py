@@ -104,7 +104,8 @@ KV_SIDE = ("K", "V", "UK", "UV")
 def test_multi_query_at_full_size(name):
     """The multi-query workloads of the benchmark (B1, 16 query heads sharing
     one key/value head, N = 16384, d = 128), run as the benchmark runs them
-    (its column kernels then take the two-wave-set form).  Row-owned outputs
+    (its column kernels then split each column block over several
+    workgroups, with a workspace and a reduction).  Row-owned outputs
     on 32 sampled query rows of every head against the oracle; column-owned
     outputs (Kt, Vt, dK, dV) on 64 sampled key rows, against the oracle's
     column slices summed over the 16 query heads, given the GPU's row scalars
