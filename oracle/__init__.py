@@ -27,6 +27,7 @@ from .bob_oracle import (  # noqa: F401
     bob_affine,
     bob_threepass,
     row_scalars,
+    row_scalars_slab,
     bob_cols,
     bob_gqa,
     expand_kv,

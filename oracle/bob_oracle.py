@@ -378,16 +378,62 @@ def bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal=False):
     )
 
 
-def row_scalars(q, k, v, do, uq, uk, uv, tau, slab=1024, causal=False):
+def row_scalars_slab(q, k, v, do, uq, uk, uv, tau, rows, causal=False):
+    """L, D, alpha, E of one head at the query rows `rows` only.
+
+    The same step functions as bob_rows (each row scalar is a sum over the
+    columns of one fixed row, Sec. 3.2), without the row-owned matrix outputs
+    that bob_rows also forms."""
+    rows = np.asarray(rows)
+    qi, doi, uqi = q[rows], do[rows], uq[rows]
+    S = scores(qi, k, tau, causal, q_idx=rows)
+    L = log_normalizer(S)
+    P = probabilities(S, L)
+    del S
+    dP = dP_of(doi, v)
+    D = row_D(P, dP)
+    F = F_of(qi, k, uqi, uk, tau)
+    alpha = alpha_of(P, F)
+    C = C_of(doi, uv)
+    Pt = Ptilde_of(C, F, dP, D, alpha)
+    E = E_of(P, Pt)
+    return dict(alpha=alpha, E=E, L=L, D=D)
+
+
+def row_scalars(q, k, v, do, uq, uk, uv, tau, slab=1024, causal=False, workers=1, progress=None):
     """alpha, E, L, D for every query row of one head, computed slab by slab
-    with bob_rows (row-owned, so slabs are exact)."""
+    with row_scalars_slab (row-owned, so slabs are exact).
+
+    workers > 1 runs the slabs in that many threads (NumPy releases the GIL
+    inside its array operations; BLAS is held to one thread per slab meanwhile).
+    Slabs and threads change nothing but the BLAS's summation order.
+    progress, if given, is called as progress(rows_done, n) after each slab."""
+    import threading
     n = q.shape[0]
     out = {key: np.empty(n) for key in ("alpha", "E", "L", "D")}
-    for r0 in range(0, n, slab):
+    starts = list(range(0, n, slab))
+    done = [0]
+    lock = threading.Lock()
+
+    def one(r0):
         rows = np.arange(r0, min(n, r0 + slab))
-        part = bob_rows(q, k, v, do, uq, uk, uv, tau, rows, causal)
+        part = row_scalars_slab(q, k, v, do, uq, uk, uv, tau, rows, causal)
         for key in out:
             out[key][rows] = part[key]
+        if progress is not None:
+            with lock:
+                done[0] += len(rows)
+                progress(done[0], n)
+
+    if workers <= 1:
+        for r0 in starts:
+            one(r0)
+        return out
+    from concurrent.futures import ThreadPoolExecutor
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1, user_api="blas"), ThreadPoolExecutor(max_workers=workers) as pool:
+        for fut in [pool.submit(one, r0) for r0 in starts]:
+            fut.result()
     return out
 
 

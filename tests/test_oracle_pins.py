@@ -387,3 +387,19 @@ def test_column_slices_match_full():
     part = bo.bob_cols(*args, tau, cols, rs["alpha"], rs["E"], rs["L"], rs["D"])
     for key in ("Kt", "Vt", "dK", "dV"):
         assert rel(part[key], full[key][cols]) < 1e-13, key
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_threaded_row_scalars_match_full(causal):
+    """row_scalars over uneven slabs in several threads gives the full
+    materialised bob_head's alpha, E, L, D, and reports every row once."""
+    rng = np.random.default_rng(17)
+    n, d = 101, 8
+    args = rand_inputs(n, d, rng)
+    tau = 1 / np.sqrt(d)
+    full = bo.bob_head(*args, tau, causal=causal)
+    seen = []
+    rs = bo.row_scalars(*args, tau, slab=7, causal=causal, workers=4, progress=lambda k, m: seen.append((k, m)))
+    for key in ("alpha", "E", "L", "D"):
+        assert rel(rs[key], full[key]) < 1e-13, key
+    assert sorted(k for k, _ in seen)[-1] == n and all(m == n for _, m in seen) and len(seen) == -(-n // 7)
