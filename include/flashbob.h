@@ -33,9 +33,9 @@
  *  pointers  device pointers owned by the caller, 16-byte aligned, on the
  *          current HIP device (the kernels run there).  The library
  *          allocates no memory (the *_ws calls take their workspace from
- *          the caller); its only state is the modes set by
- *          bob_set_column_wave_sets and bob_set_column_split and a
- *          per-device count of compute units.
+ *          the caller) and keeps no state: every choice it makes depends
+ *          only on the arguments and on the current device's compute-unit
+ *          count, so the entry points are thread-safe.
  *          Outputs must not alias inputs.
  *  stream  a hipStream_t of the current device passed as void* (NULL = the
  *          default stream).  Work
@@ -71,6 +71,46 @@ typedef enum {
   BOB_ELAUNCH = 3
 } bob_status;
 
+/* Layout of a column-owned kernel: the first backward's dK, dV kernel or
+ * Pass 2's Kt, Vt kernel (bob_column_layout: BOB_COLUMNS_BWD,
+ * BOB_COLUMNS_PASS2).  Each such kernel owns one block of key rows per
+ * workgroup and streams every query tile of the block's query heads past it
+ * (Alg. 1 Pass 2), so each output element is one long fp32 sum.  Requests
+ * (0 = automatic in every field):
+ *  parts        workgroups that share one column block, 1..8.  With more than
+ *               one, each part sums an equal share of the block's streamed
+ *               tiles and stores fp32 partial sums to the caller's workspace,
+ *               and a second kernel adds them in part order (for grids too
+ *               small, or too uneven under the causal mask, to fill the
+ *               device).  Automatic: causal grids to about 8 workgroups per
+ *               compute unit, dense Pass 2 grids smaller than the compute-unit
+ *               count to 2 per unit, the dense first backward to 8 per unit;
+ *               never for blocks of fewer than 1024 streamed tiles.
+ *  wave_sets    1 or 2 wave sets per workgroup; two take alternate streamed
+ *               tiles and add their fp32 sums through LDS at the end.
+ *               Automatic: two when the grid has no more workgroups than the
+ *               device has compute units (and the shape has room: bf16
+ *               d <= 128, fp32 Pass 2 with d <= 64); a split block uses one.
+ *  flush_tiles  streamed tiles per accumulation section, >= 1, or -1 for one
+ *               section.  The MFMA's fp32 accumulation drops the low bits of
+ *               small addends toward one side, so a chain of tens of
+ *               thousands of tiles into one accumulator drifts (the zero
+ *               column sums of Kt, Vt, dK grow with N); in sections, each
+ *               chain restarts from zero and is added into fp32 sums with
+ *               round-to-nearest adds.  Automatic: sections of 1024 tiles
+ *               when a chain would exceed 8192 tiles (bf16 d <= 128; other
+ *               (dtype, d) run one section, and asking for sections there
+ *               gives BOB_EUNSUPPORTED).
+ * Different layouts sum in different orders, so results differ in the last
+ * bits; each layout is deterministic. */
+typedef struct {
+  int32_t parts;
+  int32_t wave_sets;
+  int32_t flush_tiles;
+} bob_column_opts;
+
+enum { BOB_COLUMNS_BWD = 0, BOB_COLUMNS_PASS2 = 1 };
+
 /* Forward attention (eq. 1) with its log-normalizer (Sec. 2).
  * In:  Q, K, V  [B,H,N,d].
  * Out: O = softmax(scale Q K^T) V  [B,H,N,d];  L (fp32 [B,H,N]). */
@@ -82,7 +122,8 @@ int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, 
  * In:  Q, K, V, O, dO [B,H,N,d];  L fp32 [B,H,N] from attn_fwd_lse.
  * Out: dQ, dK, dV [B,H,N,d];  D fp32 [B,H,N], D_i = do_i . o_i.
  * D is written by the row kernel before the column kernel reads it (both
- * are enqueued on `stream` by this call). */
+ * are enqueued on `stream` by this call).  The column kernel runs unsplit
+ * with automatic wave sets and sections (bob_column_opts {1, 0, 0}). */
 int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                  const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* L, void* dQ, void* dK, void* dV, float* D, void* stream);
@@ -105,7 +146,9 @@ int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
 
 /* BoB Pass 2, column-major (Alg. 1 Pass 2).
  * In:  Q, K, V, dO, gdQ, gdK, gdV [B,H,N,d];  L, D, alpha, E fp32 [B,H,N].
- * Out: Kt, Vt [B,H,N,d].  Must run after Pass 1 has written alpha and E. */
+ * Out: Kt, Vt [B,H,N,d].  Must run after Pass 1 has written alpha and E.
+ * Runs unsplit with automatic wave sets and sections (bob_column_opts
+ * {1, 0, 0}). */
 int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                             const void* Q, const void* K, const void* V, const void* dO,
                             const void* gdQ, const void* gdK, const void* gdV,
@@ -142,51 +185,51 @@ int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
                                 const float* L, const float* D, const float* alpha, const float* E, void* Kt,
                                 void* Vt, void* stream);
 
-/* Pass 2 with each key/value column block split over several workgroups,
- * for grids too small to fill the device.  Under the causal mask a column
- * block's work is proportional to the query tiles at or below its diagonal,
- * so with few key/value heads (e.g. multi-query attention) the first blocks
- * would set the time; split, every part takes an equal share of its block's
- * (query head, query tile) iterations and stores fp32 partial Kt and Vt to
- * `workspace`, and a second kernel on the same stream adds the parts in
- * part order and writes Kt, Vt.
- * Arguments as attn_bob_pass2_cols_gqa, plus:
+/* Pass 2 and the first backward with their column kernels laid out by
+ * `opts` (bob_column_opts; NULL = all automatic), which may split a column
+ * block over workgroups and then needs a workspace.
+ * Arguments as attn_bob_pass2_cols_gqa / attn_bwd_gqa, plus:
+ *  opts    the caller's layout requests (read during the call only).
  *  workspace, workspace_bytes  device memory owned by the caller, 16-byte
- *          aligned, of at least bob_pass2_workspace_bytes() bytes for this
- *          problem; it needs no initial contents and holds nothing useful
- *          afterwards.  It must not be reused before the call's kernels have
- *          finished on `stream`.
- * When bob_pass2_workspace_bytes() is 0 the call runs the unsplit kernels
- * and ignores workspace (it may be NULL).  Otherwise a NULL, misaligned or
- * too small workspace gives BOB_EINVAL.  Split and unsplit results differ by
- * the order of the fp32 sums; each is deterministic. */
+ *          aligned, of at least bob_pass2_workspace_bytes() /
+ *          bob_bwd_workspace_bytes() for the same problem and opts; it needs
+ *          no initial contents and holds nothing useful afterwards.  It
+ *          must not be reused before the call's kernels have finished on
+ *          `stream`.  When that size is 0 (the layout does not split) the
+ *          workspace is ignored and may be NULL; otherwise a NULL,
+ *          misaligned or too small workspace gives BOB_EINVAL.
+ * A request out of range (parts outside 0..8, wave_sets outside 0..2,
+ * flush_tiles below -1) gives BOB_EINVAL.  dQ and D of the first backward do
+ * not depend on the layout. */
 int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
                                    float scale, int32_t causal, const void* Q, const void* K, const void* V,
                                    const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                                    const float* L, const float* D, const float* alpha, const float* E, void* Kt,
-                                   void* Vt, void* workspace, int64_t workspace_bytes, void* stream);
-
-/* The first backward with its column kernel (dK, dV) split the same way:
- * arguments as attn_bwd_gqa plus workspace and workspace_bytes, with the
- * rules of attn_bob_pass2_cols_gqa_ws (its size from
- * bob_bwd_workspace_bytes).  dQ and D do not depend on the split. */
+                                   void* Vt, const bob_column_opts* opts, void* workspace, int64_t workspace_bytes,
+                                   void* stream);
 int32_t attn_bwd_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
                         int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
-                        const float* L, void* dQ, void* dK, void* dV, float* D, void* workspace,
-                        int64_t workspace_bytes, void* stream);
+                        const float* L, void* dQ, void* dK, void* dV, float* D, const bob_column_opts* opts,
+                        void* workspace, int64_t workspace_bytes, void* stream);
 
-/* Workspace bytes attn_bwd_gqa_ws needs, as bob_pass2_workspace_bytes (the
- * first backward's column workgroups own their own number of key rows, so
- * the part count can differ from Pass 2's). */
-int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
-                                int32_t causal);
-
-/* Workspace bytes attn_bob_pass2_cols_gqa_ws needs for this problem on the
- * current device under the current bob_set_column_split mode: 0 when it
- * would not split (and for an empty or invalid problem, which that call
- * reports), else parts x 2 x B x Hkv x N x d x 4. */
+/* Workspace bytes attn_bob_pass2_cols_gqa_ws / attn_bwd_gqa_ws need for this
+ * problem and opts on the current device: 0 when the layout does not split
+ * (and for an empty or invalid problem or request, which the calls report),
+ * else parts x 2 x B x Hkv x N x d x 4. */
 int64_t bob_pass2_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
-                                  int32_t causal);
+                                  int32_t causal, const bob_column_opts* opts);
+int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                int32_t causal, const bob_column_opts* opts);
+
+/* The layout a column kernel (kernel: BOB_COLUMNS_BWD or BOB_COLUMNS_PASS2)
+ * would run for this problem and opts on the current device: `resolved`
+ * (may be NULL) receives parts >= 1, wave_sets (1 or 2) and flush_tiles
+ * (-1 for one section), `workspace_bytes` (may be NULL) the workspace the
+ * *_ws call needs.  Returns BOB_OK, or the status the call would return
+ * for the problem and opts (pointers aside). */
+int32_t bob_column_layout(int32_t kernel, int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                          int32_t causal, const bob_column_opts* opts, bob_column_opts* resolved,
+                          int64_t* workspace_bytes);
 
 /* Three-pass control schedule (App. "Three-pass versus two-pass" and the
  * three-pass overlay of App. "Dependency graphs"): the schedule that the
@@ -221,28 +264,6 @@ const char* bob_status_string(int32_t status);
 
 /* Static version string of the library. */
 const char* bob_version(void);
-
-/* How the column-owned kernels (the dK, dV half of attn_bwd, and Pass 2)
- * spread a key/value column block over a CU.  By default (mode 0) a column
- * block whose grid has no more workgroups than the device has compute units
- * (few key/value heads and short sequences, e.g. multi-query attention) is
- * given two wave sets in one workgroup, which take alternate streamed tiles
- * and add their fp32 partial sums in a fixed order at the end; larger grids
- * use one set.  Mode 1 always uses one set, mode 2 uses two wherever the
- * launch shape has room (bf16 d <= 128, fp32 Pass 2 with d <= 64).  The two
- * forms sum in different orders, so their results differ by rounding; for a
- * given mode, device and problem the result is deterministic.  Process-wide
- * (all devices); not ordered against launches in flight.  Returns BOB_OK, or
- * BOB_EINVAL for a mode outside 0..2. */
-int32_t bob_set_column_wave_sets(int32_t mode);
-
-/* How many workgroups attn_bwd_gqa_ws and attn_bob_pass2_cols_gqa_ws give
- * each column block.  0 (default): automatic, from the column grid, the
- * device's compute units and the mask; 1: never split; 2..8: always that
- * many parts.  Process-wide (all devices); read by the *_workspace_bytes
- * queries and by the calls themselves, which must see the same mode.  Returns BOB_OK, or BOB_EINVAL for a value
- * outside 0..8. */
-int32_t bob_set_column_split(int32_t parts);
 
 #ifdef __cplusplus
 }

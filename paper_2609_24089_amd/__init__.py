@@ -18,8 +18,21 @@ LIB_PATH = os.path.join(HERE, "libflashbob.so")
 BOB_F32 = 0
 BOB_BF16 = 1
 BOB_OK, BOB_EINVAL, BOB_EUNSUPPORTED, BOB_ELAUNCH = 0, 1, 2, 3
+BOB_COLUMNS_BWD, BOB_COLUMNS_PASS2 = 0, 1
 
 _lib = None
+
+
+class ColumnOpts(ctypes.Structure):
+    """bob_column_opts: layout requests for the column kernels (the first
+    backward's dK, dV and Pass 2's Kt, Vt); 0 = automatic in every field.
+    parts: workgroups per column block (1..8); wave_sets: 1 or 2;
+    flush_tiles: streamed tiles per accumulation section (>= 1, or -1 for
+    one section).  See include/flashbob.h."""
+    _fields_ = [("parts", ctypes.c_int32), ("wave_sets", ctypes.c_int32), ("flush_tiles", ctypes.c_int32)]
+
+    def __repr__(self):
+        return f"ColumnOpts(parts={self.parts}, wave_sets={self.wave_sets}, flush_tiles={self.flush_tiles})"
 
 
 def load_library():
@@ -55,17 +68,17 @@ def load_library():
     lib.bob_status_string.restype = ctypes.c_char_p
     lib.bob_version.argtypes = []
     lib.bob_version.restype = ctypes.c_char_p
-    lib.bob_set_column_wave_sets.argtypes = [i32]
-    lib.bob_set_column_wave_sets.restype = i32
-    lib.bob_set_column_split.argtypes = [i32]
-    lib.bob_set_column_split.restype = i32
-    lib.bob_pass2_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32]
+    opts_p = ctypes.POINTER(ColumnOpts)
+    lib.bob_pass2_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32, opts_p]
     lib.bob_pass2_workspace_bytes.restype = i64
-    lib.attn_bob_pass2_cols_gqa_ws.argtypes = common_gqa + [vp] * 13 + [vp, i64] + [vp]
-    lib.attn_bob_pass2_cols_gqa_ws.restype = i32
-    lib.bob_bwd_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32]
+    lib.bob_bwd_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64, i32, opts_p]
     lib.bob_bwd_workspace_bytes.restype = i64
-    lib.attn_bwd_gqa_ws.argtypes = common_gqa + [vp] * 10 + [vp, i64] + [vp]
+    lib.bob_column_layout.argtypes = [i32, i32, i64, i64, i64, i64, i64, i32, opts_p, opts_p,
+                                      ctypes.POINTER(i64)]
+    lib.bob_column_layout.restype = i32
+    lib.attn_bob_pass2_cols_gqa_ws.argtypes = common_gqa + [vp] * 13 + [opts_p, vp, i64] + [vp]
+    lib.attn_bob_pass2_cols_gqa_ws.restype = i32
+    lib.attn_bwd_gqa_ws.argtypes = common_gqa + [vp] * 10 + [opts_p, vp, i64] + [vp]
     lib.attn_bwd_gqa_ws.restype = i32
     _lib = lib
     return lib
@@ -75,21 +88,32 @@ def status_string(rc):
     return load_library().bob_status_string(int(rc)).decode()
 
 
-def set_column_wave_sets(mode):
-    """bob_set_column_wave_sets: 0 automatic (default), 1 one wave set per
-    column block, 2 two wherever the launch shape has room."""
-    rc = load_library().bob_set_column_wave_sets(int(mode))
-    if rc != BOB_OK:
-        raise ValueError(f"bob_set_column_wave_sets({mode}): {status_string(rc)}")
+def _opts(columns):
+    """A ColumnOpts (or None, all automatic) as the pointer argument of the
+    *_ws calls and queries."""
+    if columns is None:
+        return None
+    if not isinstance(columns, ColumnOpts):
+        raise TypeError("columns must be a ColumnOpts or None")
+    return ctypes.byref(columns)
 
 
-def set_column_split(parts):
-    """bob_set_column_split: 0 automatic (default), 1 never split a column
-    block of the first backward or Pass 2 over workgroups, 2..8 always split
-    it into that many."""
-    rc = load_library().bob_set_column_split(int(parts))
+def column_layout(kernel, dtype, B, H, Hkv, N, d, causal=False, columns=None, device=None):
+    """bob_column_layout: the layout the column kernel `kernel`
+    (BOB_COLUMNS_BWD or BOB_COLUMNS_PASS2) runs for this problem and request
+    on `device` (default: the current device).  Returns (ColumnOpts with the
+    resolved parts, wave_sets, flush_tiles (-1: one section), workspace
+    bytes)."""
+    lib = load_library()
+    code = _dtype_code(torch.empty(0, dtype=dtype))
+    got = ColumnOpts()
+    nbytes = ctypes.c_int64(0)
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        rc = lib.bob_column_layout(kernel, code, B, H, Hkv, N, d, int(bool(causal)), _opts(columns),
+                                   ctypes.byref(got), ctypes.byref(nbytes))
     if rc != BOB_OK:
-        raise ValueError(f"bob_set_column_split({parts}): {status_string(rc)}")
+        raise RuntimeError(status_string(rc))
+    return got, nbytes.value
 
 
 def _dtype_code(t):
@@ -160,13 +184,13 @@ def _call(like, fn, *args):
         raise RuntimeError(status_string(rc))
 
 
-def _column_workspace(query, code, B, H, Hkv, N, d, causal, like, stream):
+def _column_workspace(query, code, B, H, Hkv, N, d, causal, columns, like, stream):
     """(workspace, bytes) for a *_ws call whose column blocks the library
     would split over workgroups (query: its bob_*_workspace_bytes), else
     (None, 0).  The fp32 partial sums go to a buffer from torch's allocator,
     kept from reuse until the kernels on `stream` are done."""
     with torch.cuda.device(like.device):
-        nbytes = query(code, B, H, Hkv, N, d, causal)
+        nbytes = query(code, B, H, Hkv, N, d, causal, _opts(columns))
     if nbytes <= 0:
         return None, 0
     ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
@@ -197,8 +221,9 @@ def attn_fwd_lse(Q, K, V, scale, causal=False, out=None, stream=None):
     return O, L
 
 
-def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
-    """First backward (eqs. 2-3): returns (dQ, dK, dV, D); dK, dV have K's shape."""
+def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None, columns=None):
+    """First backward (eqs. 2-3): returns (dQ, dK, dV, D); dK, dV have K's shape.
+    columns: ColumnOpts for the dK, dV kernel (None: automatic)."""
     B, H, Hkv, N, d = _check_groups((Q, O, dO), (K, V))
     _check_rows(Q.shape, L)
     if out is None:
@@ -211,13 +236,9 @@ def attn_bwd(Q, K, V, O, dO, L, scale, causal=False, out=None, stream=None):
     code, c = _dtype_code(Q), int(bool(causal))
     ptrs = (_p(Q), _p(K), _p(V), _p(O), _p(dO), _p(L), _p(dQ), _p(dK), _p(dV), _p(D))
     st = _stream(stream, Q)
-    ws, nbytes = _column_workspace(lib.bob_bwd_workspace_bytes, code, B, H, Hkv, N, d, c, Q, stream)
-    if ws is not None:
-        _call(Q, lib.attn_bwd_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _p(ws), nbytes, st)
-    elif Hkv == H:
-        _call(Q, lib.attn_bwd, code, B, H, N, d, float(scale), c, *ptrs, st)
-    else:
-        _call(Q, lib.attn_bwd_gqa, code, B, H, Hkv, N, d, float(scale), c, *ptrs, st)
+    ws, nbytes = _column_workspace(lib.bob_bwd_workspace_bytes, code, B, H, Hkv, N, d, c, columns, Q, stream)
+    _call(Q, lib.attn_bwd_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _opts(columns),
+          None if ws is None else _p(ws), nbytes, st)
     return dQ, dK, dV, D
 
 
@@ -247,8 +268,10 @@ def attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal=False
     return Qt, dOt, alpha, E
 
 
-def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal=False, out=None, stream=None):
-    """BoB Pass 2 (column-major): returns (Kt, Vt), with K's shape."""
+def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal=False, out=None, stream=None,
+                        columns=None):
+    """BoB Pass 2 (column-major): returns (Kt, Vt), with K's shape.
+    columns: ColumnOpts for its layout (None: automatic)."""
     B, H, Hkv, N, d = _check_groups((Q, dO, gdQ), (K, V, gdK, gdV))
     _check_rows(Q.shape, L, D, alpha, E)
     if out is None:
@@ -260,14 +283,9 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
     ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
             _p(Kt), _p(Vt))
     st = _stream(stream, Q)
-    ws, nbytes = _column_workspace(lib.bob_pass2_workspace_bytes, code, B, H, Hkv, N, d, c, Q, stream)
-    if ws is not None:
-        _call(Q, lib.attn_bob_pass2_cols_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _p(ws), nbytes,
-              st)
-    elif Hkv == H:
-        _call(Q, lib.attn_bob_pass2_cols, code, B, H, N, d, float(scale), c, *ptrs, st)
-    else:
-        _call(Q, lib.attn_bob_pass2_cols_gqa, code, B, H, Hkv, N, d, float(scale), c, *ptrs, st)
+    ws, nbytes = _column_workspace(lib.bob_pass2_workspace_bytes, code, B, H, Hkv, N, d, c, columns, Q, stream)
+    _call(Q, lib.attn_bob_pass2_cols_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _opts(columns),
+          None if ws is None else _p(ws), nbytes, st)
     return Kt, Vt
 
 
@@ -299,32 +317,35 @@ def attn_bob3_rows(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, scale, causal=False,
     return Qt, dOt, E
 
 
-def bob3(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, stream=None):
+def bob3(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, stream=None, columns=None):
     """Whole path with the three-pass control schedule: forward, first
     backward, sweep 1 (alpha), sweep 2 (Qt, dOt, E), sweep 3 (Kt, Vt).
     Returns the same dict as bob()."""
     O, L = attn_fwd_lse(Q, K, V, scale, causal, stream=stream)
-    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream, columns=columns)
     alpha = attn_bob3_alpha_rows(Q, K, gdQ, gdK, L, scale, causal, stream=stream)
     Qt, dOt, E = attn_bob3_rows(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, scale, causal, stream=stream)
-    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream)
+    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream,
+                                 columns=columns)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)
 
 
-def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, use_dq=True, stream=None):
+def bob(Q, K, V, dO, gdQ, gdK, gdV, scale, causal=False, use_dq=True, stream=None, columns=None):
     """Whole path: forward, first backward, Pass 1, Pass 2 on one stream.
 
     use_dq=True hands the first-backward dQ to Pass 1 (five-accumulator form);
-    use_dq=False runs the six-accumulator form of Prop. 3.1.
+    use_dq=False runs the six-accumulator form of Prop. 3.1.  columns: a
+    ColumnOpts for both column kernels (None: automatic).
 
     Returns a dict with Qt, Kt, Vt, dOt, alpha, E and the producer state
     O, L, D, dQ, dK, dV.
     """
     O, L = attn_fwd_lse(Q, K, V, scale, causal, stream=stream)
-    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream)
+    dQ, dK, dV, D = attn_bwd(Q, K, V, O, dO, L, scale, causal, stream=stream, columns=columns)
     Qt, dOt, alpha, E = attn_bob_pass1_rows(Q, K, V, O, dO, gdQ, gdK, gdV, L, D, scale, causal,
                                             dQ=dQ if use_dq else None, stream=stream)
-    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream)
+    Kt, Vt = attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal, stream=stream,
+                                 columns=columns)
     return dict(Qt=Qt, Kt=Kt, Vt=Vt, dOt=dOt, alpha=alpha, E=E, O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV)
 
 

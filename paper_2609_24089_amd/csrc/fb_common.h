@@ -536,6 +536,59 @@ __device__ __forceinline__ void store_column_part(float* parts_out, int64_t plan
   }
 }
 
+// Two-level accumulation for the key-side sums of a column kernel (kOn).
+// A column block's Kt/Vt (or dK/dV) sums run over every streamed query tile,
+// G * N / 32 MFMA steps into one fp32 accumulator.  The MFMA's own fp32
+// accumulation is not round-to-nearest: when the accumulator is far larger
+// than one step's products it loses their low bits toward one side, and that
+// one-signed error grows with the chain (measured: the zero column sums
+// sum_j Kt_j = 0 drift from 3e-3 at N = 2^19 to 3e-2 at N = 2^21, and the
+// residual falls in proportion to the chain when it is cut).  With kOn the
+// MFMA chain runs `every` streamed tiles, is added into fp32 section sums
+// by ordinary (round-to-nearest) VALU adds, and restarts from zero; finish()
+// adds the last partial section.  x, y are [16-dim block][stationary block].
+template <bool kOn, int A, int B>
+struct SectionSums {
+  floatx4 sx[kOn ? A : 1][kOn ? B : 1], sy[kOn ? A : 1][kOn ? B : 1];
+  int n;
+  __device__ __forceinline__ void init() {
+    n = 0;
+    if constexpr (kOn) {
+#pragma unroll
+      for (int a = 0; a < A; ++a)
+#pragma unroll
+        for (int b = 0; b < B; ++b) sx[a][b] = sy[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  // after the accumulate MFMAs of one streamed tile
+  __device__ __forceinline__ void step(floatx4 (&x)[A][B], floatx4 (&y)[A][B], int every) {
+    if constexpr (kOn) {
+      if (++n == every) {
+        n = 0;
+#pragma unroll
+        for (int a = 0; a < A; ++a)
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+            sx[a][b] += x[a][b];
+            sy[a][b] += y[a][b];
+            x[a][b] = y[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+    }
+  }
+  __device__ __forceinline__ void finish(floatx4 (&x)[A][B], floatx4 (&y)[A][B]) {
+    if constexpr (kOn) {
+#pragma unroll
+      for (int a = 0; a < A; ++a)
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          x[a][b] = sx[a][b] + x[a][b];
+          y[a][b] = sy[a][b] + y[a][b];
+        }
+    }
+  }
+};
+
 // Two wave sets of one workgroup that accumulated the same stationary rows
 // over disjoint sets of streamed tiles: set 1 hands its fp32 accumulators x,
 // then y, to set 0 through LDS (buf: every wave's A*B 1 KB blocks, placed by

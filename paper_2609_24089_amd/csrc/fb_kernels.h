@@ -282,12 +282,13 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // are added through LDS at the end (KS = 2 fills a CU when the grid has no
 // more workgroups than CUs).
 // ===========================================================================
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kParts = false>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kParts = false,
+          bool kFlush = false>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
     T* __restrict__ dK, T* __restrict__ dV, int N, int nRB, int total, float scale, int causal, int grp,
-    float* __restrict__ parts_out = nullptr, int nparts = 1) {
+    float* __restrict__ parts_out = nullptr, int nparts = 1, int flush_tiles = 0) {
   static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
@@ -327,6 +328,8 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   for (int nb = 0; nb < G::kNB; ++nb)
 #pragma unroll
     for (int mc = 0; mc < MC; ++mc) dk[nb][mc] = dv[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+  SectionSums<kFlush, G::kNB, MC> sect;
+  sect.init();
   const float c = scale * kLog2e;
   floatx4 s[2][MC], dp[2][MC];
   typename E::TFrag pf[MC], dsf[MC];
@@ -422,8 +425,10 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
             dk[nb][mc] = E::mma_acc(aq, dsf[mc], dk[nb][mc]);
           }
         }
+        sect.step(dk, dv, flush_tiles);
         prep_next();
       });
+  sect.finish(dk, dv);
   if constexpr (KS == 2) {
     static_assert(sizeof(lds) >= (size_t)NW * G::kNB * MC * 1024, "set merge buffer");
     merge_wave_sets(dk, dv, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);
@@ -805,14 +810,14 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
 // them); the grid then holds total * nparts jobs (map_column_job).
 // ===========================================================================
 template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kPF,
-          bool kParts = false>
+          bool kParts = false, bool kFlush = false>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
     const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
     const float* __restrict__ alpha_in, const float* __restrict__ E_in,
     T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp,
-    float* __restrict__ parts_out = nullptr, int nparts = 1) {
+    float* __restrict__ parts_out = nullptr, int nparts = 1, int flush_tiles = 0) {
   static_assert(KS == 1 || KS == 2, "wave sets");
   using E = Elt<T>;
   using G = Geo<T, D>;
@@ -859,6 +864,8 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   for (int nb = 0; nb < G::kNB; ++nb)
 #pragma unroll
     for (int mc = 0; mc < MC; ++mc) aK[nb][mc] = aV[nb][mc] = floatx4{0.f, 0.f, 0.f, 0.f};
+  SectionSums<kFlush, G::kNB, MC> sect;
+  sect.init();
   const float c = scale * kLog2e;
   floatx4 s[2][MC], dp[2][MC], f[2][MC], cc[2][MC];
   typename E::TFrag fPh[MC], fSt[MC], fdS[MC];
@@ -1024,7 +1031,9 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
             aK[nb][mc] = E::mma_acc(auq, fdS[mc], aK[nb][mc]);
           }
         }
+        sect.step(aK, aV, flush_tiles);
       });
+  sect.finish(aK, aV);
   if constexpr (KS == 2) {
     static_assert(sizeof(lds) >= (size_t)NW * G::kNB * MC * 1024, "set merge buffer");
     merge_wave_sets(aK, aV, ks, wl, (floatx4 FB_LDS*)&lds[0][0][0]);

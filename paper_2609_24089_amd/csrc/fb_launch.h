@@ -6,7 +6,6 @@
 // extern template declarations at the end.
 #pragma once
 #include <algorithm>
-#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <initializer_list>
@@ -22,44 +21,55 @@ namespace fb {
 // LDS pipeline stages (tiles in flight + 1), DS = workgroups that share one
 // row block, each accumulating 1/DS of the head dims (Pass 1 only), PF = 1 to
 // read the accumulate operands one block ahead (Pass 1 and Pass 2).
+// kColsF and kP2F are the shapes of the column kernels' two-level
+// (sectioned) accumulation for long streams (SectionSums), which holds a
+// second set of key-side sums; mr = 0 where that form is not built.
 struct Shape {
   int mr, nw, occ, st, ds = 1, pf = 0;
 };
+constexpr Shape kNoForm{0, 1, 1, 2};
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 32> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{2, 4, 2, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
+  static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2};
 };
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{2, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{1, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
   static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1};
 };
 template <> struct Cfg<bf16, 256> {
   static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
 };
 template <> struct Cfg<float, 32> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
 };
 template <> struct Cfg<float, 64> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
 };
 template <> struct Cfg<float, 128> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -127,21 +137,52 @@ inline Grid grid_for(const Problem& p, int rows_per_block, bool kv_heads = false
   return g;
 }
 
-// Compute units of the current device (0 if it cannot be read), read once per
-// device.
+// ---------------------------------------------------------------------------
+// Column kernels (the first backward's dK, dV and Pass 2's Kt, Vt): how one
+// problem's column blocks are laid out over workgroups.
+//  * parts: workgroups per column block (kParts forms; 1 = unsplit).  Split,
+//    each part stores fp32 partial sums to a caller's workspace and
+//    bob_column_parts_reduce_kernel adds them.
+//  * sets: wave sets per workgroup (KS = 2 fills a CU with one workgroup when
+//    the grid has no more workgroups than the device has CUs; shapes held to
+//    two waves per SIMD whose two LDS rings fit 160 KB and hold the merge
+//    buffer).
+//  * flush_tiles: streamed tiles per MFMA accumulation section (SectionSums;
+//    0 = one chain over the whole stream), with the kColsF / kP2F shape.
+// The caller's requests (bob_column_opts; 0 = automatic) are resolved here,
+// deterministically from the problem and the device's CU count, so the
+// workspace query and the call that uses the workspace agree.
+// ---------------------------------------------------------------------------
+constexpr int kMaxParts = 8;
+// Automatic sections: a stream longer than kLongChain tiles per accumulator
+// chain is cut into sections of kSectionTiles.  Measured on the zero column
+// sums (B1 H1 d64 bf16): at chains of 8192 tiles the residual stays at the
+// bf16 rounding floor, at 32768 and above it is over three times the floor.
+constexpr int64_t kLongChain = 8192;
+constexpr int kSectionTiles = 1024;
+
+struct ColumnOpts {
+  int parts = 0, wave_sets = 0, flush_tiles = 0;
+};
+struct ColumnPlan {
+  Grid g{0, 0};
+  int parts = 1, sets = 1, flush_tiles = 0;
+};
+
+// Compute units of the current device (0 if it cannot be read).
 int device_cus();
 
-// Column kernels (bwd cols, Pass 2) run two wave sets per workgroup when the
-// grid has no more workgroups than the device has CUs (few key/value heads
-// times few column blocks, e.g. multi-query attention): one 4-wave workgroup
-// per CU leaves half of its wave slots empty, and the two sets split the
-// streamed tiles instead.  That applies to shapes held to two waves per SIMD
-// (a one-wave shape already fills a CU with one workgroup), and needs the two
-// LDS rings (NTENS tiles and NSCAL row scalars per stage each) to fit a
-// workgroup's 160 KB and the sets' merge buffer to fit in the rings.
-// Whether a column kernel with this many workgroups runs two wave sets, from
-// the mode set by bob_set_column_wave_sets (default: automatic).
-bool use_two_sets(int workgroups);
+// Automatic (requested = 0) or forced part count for a column grid of
+// `workgroups` with `iters` streamed iterations per block.
+int resolve_parts(int requested, int workgroups, bool causal, bool pass2, int64_t iters);
+
+// Automatic (requested = 0: two sets when the grid has no more workgroups
+// than the device has CUs) or forced (1, 2) wave sets.
+inline bool resolve_two_sets(int requested, int workgroups) {
+  if (requested == 1) return false;
+  if (requested == 2) return true;
+  return workgroups <= device_cus();
+}
 
 template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, int NTENS, int NSCAL>
 constexpr bool two_sets_fit() {
@@ -149,6 +190,57 @@ constexpr bool two_sets_fit() {
   constexpr size_t scal = (size_t)(NSTAGE + 2) * NSCAL * kBS * sizeof(float);
   return OCC == 2 && 2 * (ring + scal) <= 160 * 1024 &&
          2 * ring >= (size_t)NW * Geo<T, D>::kNB * MC * 1024;
+}
+
+// Streamed iterations of one column block: its group's query heads times
+// 32-row query tiles (the first block under the causal mask streams them all).
+inline int64_t column_iters(const Problem& p) { return (int64_t)group(p) * ((p.N + 31) / 32); }
+
+// fp32 workspace of a split column kernel: parts x {Kt, Vt} (or {dK, dV})
+// x B*Hkv*N*d.
+inline int64_t column_workspace_bytes(const Problem& p, int parts) {
+  return parts > 1 ? (int64_t)parts * 2 * p.B * p.Hkv * p.N * p.d * (int64_t)sizeof(float) : 0;
+}
+
+template <typename T, int D, bool kPass2, bool kF>
+struct ColumnShape {
+  static constexpr Shape kS =
+      kPass2 ? (kF ? Cfg<T, D>::kP2F : Cfg<T, D>::kP2) : (kF ? Cfg<T, D>::kColsF : Cfg<T, D>::kCols);
+  static constexpr bool kTwoFit =
+      kS.mr > 0 && two_sets_fit<T, D, kS.mr, kS.nw, kS.occ, kS.st, kPass2 ? 3 : 2, kPass2 ? 4 : 2>();
+};
+
+// Plan of a validated, non-empty, supported problem.  BOB_EINVAL for a
+// request out of range, BOB_EUNSUPPORTED for sections requested where the
+// sectioned form is not built.
+template <typename T, int D, bool kPass2>
+int32_t plan_columns(const Problem& p, const ColumnOpts& o, ColumnPlan* out) {
+  if (o.parts < 0 || o.parts > kMaxParts || o.wave_sets < 0 || o.wave_sets > 2 || o.flush_tiles < -1)
+    return BOB_EINVAL;
+  using S0 = ColumnShape<T, D, kPass2, false>;
+  using SF = ColumnShape<T, D, kPass2, true>;
+  auto fill = [&](const Shape& s, bool two_fit) {
+    ColumnPlan c;
+    c.g = grid_for(p, 16 * s.mr * s.nw, true);
+    c.parts = resolve_parts(o.parts, c.g.total, p.causal != 0, kPass2, column_iters(p));
+    if ((int64_t)c.g.total * c.parts > INT32_MAX) c.parts = 1;
+    c.sets = (c.parts == 1 && two_fit && resolve_two_sets(o.wave_sets, c.g.total)) ? 2 : 1;
+    return c;
+  };
+  ColumnPlan c = fill(S0::kS, S0::kTwoFit);
+  int ft = o.flush_tiles;
+  if (ft == 0) {
+    const int64_t per = (int64_t)c.parts * c.sets;
+    const int64_t chain = (column_iters(p) + per - 1) / per;
+    ft = (SF::kS.mr > 0 && chain > kLongChain) ? kSectionTiles : -1;
+  }
+  if (ft > 0) {
+    if (SF::kS.mr == 0) return BOB_EUNSUPPORTED;
+    c = fill(SF::kS, SF::kTwoFit);
+    c.flush_tiles = ft;
+  }
+  *out = c;
+  return BOB_OK;
 }
 
 template <typename T, int D>
@@ -162,11 +254,57 @@ int32_t launch_fwd(const Problem& p, const void* Q, const void* K, const void* V
   return finish_launch();
 }
 
+template <typename T, int D, bool kF>
+int32_t launch_bwd_cols(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
+                        const float* L, const float* Dv, void* dK, void* dV, hipStream_t s, const ColumnPlan& cp,
+                        float* parts_ws) {
+  constexpr Shape cc = ColumnShape<T, D, false, kF>::kS;
+  if constexpr (cc.mr == 0) {
+    return BOB_EUNSUPPORTED;
+  } else {
+    const Grid& gc = cp.g;
+    (void)hipGetLastError();
+    if (cp.parts > 1) {
+      // each column block split over cp.parts workgroups, then one reduction
+      hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true, 1, true, kF>),
+                         dim3(gc.total * cp.parts), dim3(64 * cc.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
+                         (const T*)dO, L, Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal,
+                         group(p), parts_ws, cp.parts, cp.flush_tiles);
+      const int64_t plane = p.B * p.Hkv * p.N * p.d;
+      const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
+      hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
+                         cp.parts, plane, p.scale, 1.0f, (T*)dK, (T*)dV);
+      return finish_launch();
+    }
+    auto cols = [&](auto gqa, auto ks) {
+      hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, decltype(gqa)::value,
+                                               decltype(ks)::value, false, kF>),
+                         dim3(gc.total), dim3(64 * cc.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K,
+                         (const T*)V, (const T*)dO, L, Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
+                         p.causal, group(p), (float*)nullptr, 1, cp.flush_tiles);
+    };
+    const bool gqa = group(p) != 1;
+    if constexpr (ColumnShape<T, D, false, kF>::kTwoFit) {
+      if (cp.sets == 2) {
+        gqa ? cols(std::true_type{}, std::integral_constant<int, 2>{})
+            : cols(std::false_type{}, std::integral_constant<int, 2>{});
+        return finish_launch();
+      }
+    }
+    gqa ? cols(std::true_type{}, std::integral_constant<int, 1>{})
+        : cols(std::false_type{}, std::integral_constant<int, 1>{});
+    return finish_launch();
+  }
+}
+
+// The first backward: the row kernel (dQ, D), then the column kernel (dK, dV)
+// laid out by `cp` (plan_columns<T, D, false>); parts_ws is the caller's
+// workspace when cp.parts > 1.
 template <typename T, int D>
 int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
                    const void* dO, const float* L, void* dQ, void* dK, void* dV, float* Dv,
-                   hipStream_t s, float* parts_ws = nullptr, int parts = 1) {
-  constexpr Shape cr = Cfg<T, D>::kRows, cc = Cfg<T, D>::kCols;
+                   hipStream_t s, const ColumnPlan& cp, float* parts_ws) {
+  constexpr Shape cr = Cfg<T, D>::kRows;
   const Grid gr = grid_for(p, 16 * cr.mr * cr.nw);
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_bwd_rows_kernel<T, D, cr.mr, cr.nw, cr.occ, cr.st>), dim3(gr.total), dim3(64 * cr.nw), 0, s,
@@ -174,37 +312,11 @@ int32_t launch_bwd(const Problem& p, const void* Q, const void* K, const void* V
                      (int)p.N, gr.nRB, gr.total, p.scale, p.causal, group(p));
   int32_t rc = finish_launch();
   if (rc != BOB_OK) return rc;
-  const Grid gc = grid_for(p, 16 * cc.mr * cc.nw, true);
-  const bool two = use_two_sets(gc.total);
-  (void)hipGetLastError();
-  if (parts > 1) {
-    // each column block split over `parts` workgroups, then one reduction
-    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true, 1, true>),
-                       dim3(gc.total * parts), dim3(64 * cc.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
-                       (const T*)dO, L, (const float*)Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
-                       p.causal, group(p), parts_ws, parts);
-    const int64_t plane = p.B * p.Hkv * p.N * p.d;
-    const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
-    hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
-                       parts, plane, p.scale, 1.0f, (T*)dK, (T*)dV);
-    return finish_launch();
-  }
-  auto cols = [&](auto gqa, auto ks) {
-    hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, decltype(gqa)::value, decltype(ks)::value>),
-                       dim3(gc.total), dim3(64 * cc.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V,
-                       (const T*)dO, L, (const float*)Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
-                       p.causal, group(p));
-  };
-  const bool gqa = group(p) != 1;
-  if constexpr (two_sets_fit<T, D, cc.mr, cc.nw, cc.occ, cc.st, 2, 2>()) {
-    if (two) {
-      gqa ? cols(std::true_type{}, std::integral_constant<int, 2>{}) : cols(std::false_type{}, std::integral_constant<int, 2>{});
-      return finish_launch();
-    }
-  }
-  gqa ? cols(std::true_type{}, std::integral_constant<int, 1>{}) : cols(std::false_type{}, std::integral_constant<int, 1>{});
-  return finish_launch();
+  if (cp.flush_tiles > 0)
+    return launch_bwd_cols<T, D, true>(p, Q, K, V, dO, L, Dv, dK, dV, s, cp, parts_ws);
+  return launch_bwd_cols<T, D, false>(p, Q, K, V, dO, L, Dv, dK, dV, s, cp, parts_ws);
 }
+
 
 template <typename T, int D>
 int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void* V, const void* O,
@@ -259,73 +371,62 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
   return finish_launch();
 }
 
+template <typename T, int D, bool kF>
+int32_t launch_pass2_form(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
+                          const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
+                          const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s,
+                          const ColumnPlan& cp, float* parts_ws) {
+  constexpr Shape c = ColumnShape<T, D, true, kF>::kS;
+  if constexpr (c.mr == 0) {
+    return BOB_EUNSUPPORTED;
+  } else {
+    const Grid& g = cp.g;
+    (void)hipGetLastError();
+    if (cp.parts > 1) {
+      // each column block split over cp.parts workgroups, then one reduction
+      hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, true, 1, c.pf != 0, true, kF>),
+                         dim3(g.total * cp.parts), dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
+                         (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt,
+                         (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p), parts_ws, cp.parts,
+                         cp.flush_tiles);
+      const int64_t plane = p.B * p.Hkv * p.N * p.d;
+      const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
+      hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
+                         cp.parts, plane, p.scale, p.scale, (T*)Kt, (T*)Vt);
+      return finish_launch();
+    }
+    auto pass2 = [&](auto gqa, auto ks) {
+      hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value,
+                                           c.pf != 0, false, kF>),
+                         dim3(g.total), dim3(64 * c.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K,
+                         (const T*)V, (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E,
+                         (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p), (float*)nullptr, 1,
+                         cp.flush_tiles);
+    };
+    const bool gqa = group(p) != 1;
+    if constexpr (ColumnShape<T, D, true, kF>::kTwoFit) {
+      if (cp.sets == 2) {
+        gqa ? pass2(std::true_type{}, std::integral_constant<int, 2>{})
+            : pass2(std::false_type{}, std::integral_constant<int, 2>{});
+        return finish_launch();
+      }
+    }
+    gqa ? pass2(std::true_type{}, std::integral_constant<int, 1>{})
+        : pass2(std::false_type{}, std::integral_constant<int, 1>{});
+    return finish_launch();
+  }
+}
+
+// Pass 2 laid out by `cp` (plan_columns<T, D, true>); parts_ws is the
+// caller's workspace when cp.parts > 1.
 template <typename T, int D>
 int32_t launch_pass2(const Problem& p, const void* Q, const void* K, const void* V, const void* dO,
                      const void* UQ, const void* UK, const void* UV, const float* L, const float* Dv,
-                     const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s,
-                     float* parts_ws = nullptr, int parts = 1) {
-  constexpr Shape c = Cfg<T, D>::kP2;
-  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  (void)hipGetLastError();
-  if (parts > 1) {
-    // each column block split over `parts` workgroups, then one reduction
-    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, true, 1, c.pf != 0, true>),
-                       dim3(g.total * parts), dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
-                       (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt,
-                       (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p), parts_ws, parts);
-    const int64_t plane = p.B * p.Hkv * p.N * p.d;
-    const int blocks = (int)std::min<int64_t>((plane / 2 + 255) / 256, 4096);
-    hipLaunchKernelGGL((bob_column_parts_reduce_kernel<T>), dim3(blocks), dim3(256), 0, s, (const float*)parts_ws,
-                       parts, plane, p.scale, p.scale, (T*)Kt, (T*)Vt);
-    return finish_launch();
-  }
-  const bool two = use_two_sets(g.total);
-  auto pass2 = [&](auto gqa, auto ks) {
-    hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value, c.pf != 0>), dim3(g.total),
-                       dim3(64 * c.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
-                       (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N,
-                       g.nRB, g.total, p.scale, p.causal, group(p));
-  };
-  const bool gqa = group(p) != 1;
-  if constexpr (two_sets_fit<T, D, c.mr, c.nw, c.occ, c.st, 3, 4>()) {
-    if (two) {
-      gqa ? pass2(std::true_type{}, std::integral_constant<int, 2>{}) : pass2(std::false_type{}, std::integral_constant<int, 2>{});
-      return finish_launch();
-    }
-  }
-  gqa ? pass2(std::true_type{}, std::integral_constant<int, 1>{}) : pass2(std::false_type{}, std::integral_constant<int, 1>{});
-  return finish_launch();
-}
-
-// How many workgroups share a column block of the first backward's or Pass
-// 2's column kernel (1: no split), from the mode set by
-// bob_set_column_split, the kernel's column grid and the mask.
-int column_parts(int workgroups, bool causal, bool pass2, int64_t iters_per_block);
-
-// Streamed iterations of one column block: its group's query heads times
-// 32-row query tiles (fewer under the causal mask).
-inline int64_t column_iters(const Problem& p) { return (int64_t)group(p) * ((p.N + 31) / 32); }
-
-template <typename T, int D>
-int bwd_parts(const Problem& p) {
-  constexpr Shape c = Cfg<T, D>::kCols;
-  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const int parts = column_parts(g.total, p.causal != 0, false, column_iters(p));
-  return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
-}
-
-template <typename T, int D>
-int pass2_parts(const Problem& p) {
-  constexpr Shape c = Cfg<T, D>::kP2;
-  const Grid g = grid_for(p, 16 * c.mr * c.nw, true);
-  const int parts = column_parts(g.total, p.causal != 0, true, column_iters(p));
-  return (int64_t)g.total * parts > INT32_MAX ? 1 : parts;
-}
-
-// fp32 workspace of a split column kernel: parts x {Kt, Vt} (or {dK, dV})
-// x B*Hkv*N*d.
-inline int64_t column_workspace_bytes(const Problem& p, int parts) {
-  return parts > 1 ? (int64_t)parts * 2 * p.B * p.Hkv * p.N * p.d * (int64_t)sizeof(float) : 0;
+                     const float* alpha, const float* E, void* Kt, void* Vt, hipStream_t s, const ColumnPlan& cp,
+                     float* parts_ws) {
+  if (cp.flush_tiles > 0)
+    return launch_pass2_form<T, D, true>(p, Q, K, V, dO, UQ, UK, UV, L, Dv, alpha, E, Kt, Vt, s, cp, parts_ws);
+  return launch_pass2_form<T, D, false>(p, Q, K, V, dO, UQ, UK, UV, L, Dv, alpha, E, Kt, Vt, s, cp, parts_ws);
 }
 
 // Built in fb_passes_d128.hip.
@@ -334,7 +435,7 @@ extern template int32_t launch_pass1<bf16, 128>(const Problem&, const void*, con
                                                 const float*, const void*, void*, void*, float*, float*, hipStream_t);
 extern template int32_t launch_pass2<bf16, 128>(const Problem&, const void*, const void*, const void*, const void*,
                                                 const void*, const void*, const void*, const float*, const float*,
-                                                const float*, const float*, void*, void*, hipStream_t, float*,
-                                                int);
+                                                const float*, const float*, void*, void*, hipStream_t,
+                                                const ColumnPlan&, float*);
 
 }  // namespace fb

@@ -15,6 +15,7 @@ template int32_t launch_pass1<bf16, 128>(const Problem&, const void*, const void
                                          const float*, const void*, void*, void*, float*, float*, hipStream_t);
 template int32_t launch_pass2<bf16, 128>(const Problem&, const void*, const void*, const void*, const void*,
                                          const void*, const void*, const void*, const float*, const float*,
-                                         const float*, const float*, void*, void*, hipStream_t, float*, int);
+                                         const float*, const float*, void*, void*, hipStream_t, const ColumnPlan&,
+                                         float*);
 
 }  // namespace fb

@@ -6,29 +6,16 @@
 
 namespace fb {
 
+// Compute units of the current device, read from the runtime on every call
+// (the library keeps no state of its own).
 int device_cus() {
-  static std::atomic<int> cached[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  int n = cached[dev].load(std::memory_order_relaxed);
-  if (n == 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
-    cached[dev].store(n, std::memory_order_relaxed);
-  }
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
   return n;
 }
 
-// The mode of bob_set_column_wave_sets (0 automatic, 1 one set, 2 two sets).
-static std::atomic<int> g_wave_sets{0};
-
-bool use_two_sets(int workgroups) {
-  const int mode = g_wave_sets.load(std::memory_order_relaxed);
-  if (mode == 1) return false;
-  if (mode == 2) return true;
-  return workgroups <= device_cus();
-}
-
-// Dispatch on (dtype, d) to a templated launcher.
+// Dispatch on (dtype, d) to a templated function.
 #define FB_DISPATCH(p, FN, ...)                                                  \
   do {                                                                           \
     if ((p).dtype == BOB_BF16 && (p).d == 32) return FN<fb::bf16, 32>(__VA_ARGS__);  \
@@ -41,30 +28,24 @@ bool use_two_sets(int workgroups) {
     return BOB_EUNSUPPORTED;                                                     \
   } while (0)
 
-// The mode of bob_set_column_split (0 automatic, 1 never, 2..8 that many
-// parts wherever the kernels run).
-static std::atomic<int> g_split{0};
-constexpr int kMaxParts = 8;
-
-// Automatic choice, from interleaved timing at B1 H16 N16384 d128 bf16 with
-// 1, 2, 4 and 16 key/value heads.  Causal: a column block's work grows with
-// the query tiles at or below its diagonal, and splitting until there are
-// about 8 jobs per CU made the heaviest block's share short enough to
-// balance (Pass 2 and the first backward 1.3-2x faster with 1-4 key/value
-// heads; no gain with 16).  Dense Pass 2: blocks are equal, and the only gain
-// was filling both workgroup slots of each CU on a grid smaller than the CU
-// count (6% with one key/value head, against two wave sets in one
-// workgroup).  The dense first backward gained from the same 8 jobs per CU
-// as the causal one (9-18% with 1 and 4 key/value heads).  Either kernel
+// Automatic choice (requested = 0), from interleaved timing at B1 H16 N16384
+// d128 bf16 with 1, 2, 4 and 16 key/value heads.  Causal: a column block's
+// work grows with the query tiles at or below its diagonal, and splitting
+// until there are about 8 jobs per CU made the heaviest block's share short
+// enough to balance (Pass 2 and the first backward 1.3-2x faster with 1-4
+// key/value heads; no gain with 16).  Dense Pass 2: blocks are equal, and the
+// only gain was filling both workgroup slots of each CU on a grid smaller
+// than the CU count (6% with one key/value head, against two wave sets in
+// one workgroup).  The dense first backward gained from the same 8 jobs per
+// CU as the causal one (9-18% with 1 and 4 key/value heads).  Either kernel
 // only splits blocks of at least 1024 streamed iterations (query heads per
 // group x 32-row query tiles): on the causal B4 H12 problems at N = 2048 and
 // 4096 (64 and 128 iterations), the parts' fp32 round trip through HBM cost
 // more than the balance gained (up to 14% slower), while every gain above
-// came from blocks of 2048 iterations or more.
-int column_parts(int workgroups, bool causal, bool pass2, int64_t iters_per_block) {
-  const int mode = g_split.load(std::memory_order_relaxed);
-  if (mode >= 2) return mode;
-  if (mode == 1 || workgroups <= 0 || iters_per_block < 1024) return 1;
+// came from blocks of 2048 iterations or more.  Requested 1..8: that many.
+int resolve_parts(int requested, int workgroups, bool causal, bool pass2, int64_t iters) {
+  if (requested >= 1) return requested;
+  if (workgroups <= 0 || iters < 1024) return 1;
   const int cus = device_cus();
   const bool fill_only = pass2 && !causal;
   if (cus <= 0 || (fill_only && workgroups > cus)) return 1;
@@ -73,36 +54,78 @@ int column_parts(int workgroups, bool causal, bool pass2, int64_t iters_per_bloc
   return parts < 2 ? 1 : (int)std::min<int64_t>(parts, kMaxParts);
 }
 
-// Parts of a validated, supported problem's column kernel: Pass 2's
-// (pass2 = true) or the first backward's.
-static int column_parts_of(const Problem& p, bool pass2) {
-#define FB_PARTS(TT, DD) \
-  if (p.dtype == (std::is_same<TT, float>::value ? BOB_F32 : BOB_BF16) && p.d == DD) \
-    return pass2 ? pass2_parts<TT, DD>(p) : bwd_parts<TT, DD>(p);
-  FB_PARTS(bf16, 32)
-  FB_PARTS(bf16, 64)
-  FB_PARTS(bf16, 128)
-  FB_PARTS(bf16, 256)
-  FB_PARTS(float, 32)
-  FB_PARTS(float, 64)
-  FB_PARTS(float, 128)
-#undef FB_PARTS
-  return 1;
+static ColumnOpts opts_of(const bob_column_opts* o) {
+  ColumnOpts c;
+  if (o != nullptr) {
+    c.parts = o->parts;
+    c.wave_sets = o->wave_sets;
+    c.flush_tiles = o->flush_tiles;
+  }
+  return c;
 }
 
-// Workspace of a column kernel's split for the *_ws entry points (0 when
-// it would not split, or for an empty or invalid problem).
-static int64_t column_ws_bytes(const Problem& p, bool pass2) {
+// The plain (non-_ws) entry points never split a column block: they have no
+// workspace.  Wave sets and sections are automatic.
+constexpr ColumnOpts kUnsplit{1, 0, 0};
+
+template <typename T, int D>
+int32_t plan_bwd(const Problem& p, const ColumnOpts& o, ColumnPlan* c) {
+  return plan_columns<T, D, false>(p, o, c);
+}
+template <typename T, int D>
+int32_t plan_pass2(const Problem& p, const ColumnOpts& o, ColumnPlan* c) {
+  return plan_columns<T, D, true>(p, o, c);
+}
+
+// Plan of a column kernel (pass2: Pass 2, else the first backward's) for a
+// valid problem; an empty problem gets the trivial plan.
+static int32_t column_plan(const Problem& p, bool pass2, const ColumnOpts& o, ColumnPlan* c) {
   bool empty;
-  if (check_problem(p, &empty) != BOB_OK || empty) return 0;
-  return column_workspace_bytes(p, column_parts_of(p, pass2));
+  int32_t rc = check_problem(p, &empty);
+  if (rc != BOB_OK) return rc;
+  if (empty) {
+    if (o.parts < 0 || o.parts > kMaxParts || o.wave_sets < 0 || o.wave_sets > 2 || o.flush_tiles < -1)
+      return BOB_EINVAL;
+    *c = ColumnPlan{};
+    return BOB_OK;
+  }
+  if (pass2) FB_DISPATCH(p, plan_pass2, p, o, c);
+  FB_DISPATCH(p, plan_bwd, p, o, c);
 }
 
-// The workspace checks of a *_ws entry point for a valid, non-empty problem
-// that splits into `parts` (> 1).
-static int32_t check_workspace(const Problem& p, int parts, const void* ws, int64_t bytes) {
-  if (ws == nullptr || bytes < column_workspace_bytes(p, parts) || check_ptrs({ws}) != BOB_OK) return BOB_EINVAL;
+// The workspace checks of a *_ws entry point for a plan that splits.
+static int32_t check_workspace(const Problem& p, const ColumnPlan& c, const void* ws, int64_t bytes) {
+  if (c.parts <= 1) return BOB_OK;
+  if (ws == nullptr || bytes < column_workspace_bytes(p, c.parts) || check_ptrs({ws}) != BOB_OK) return BOB_EINVAL;
   return BOB_OK;
+}
+
+static int32_t run_bwd(const Problem& p, const ColumnOpts& o, const void* Q, const void* K, const void* V,
+                       const void* O, const void* dO, const float* L, void* dQ, void* dK, void* dV, float* D,
+                       void* ws, int64_t ws_bytes, void* stream) {
+  bool empty;
+  int32_t rc = check_problem(p, &empty);
+  if (rc != BOB_OK) return rc;
+  ColumnPlan c;
+  if ((rc = column_plan(p, false, o, &c)) != BOB_OK || empty) return rc;
+  if ((rc = check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D})) != BOB_OK) return rc;
+  if ((rc = check_workspace(p, c, ws, ws_bytes)) != BOB_OK) return rc;
+  FB_DISPATCH(p, launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream, c, (float*)ws);
+}
+
+static int32_t run_pass2(const Problem& p, const ColumnOpts& o, const void* Q, const void* K, const void* V,
+                         const void* dO, const void* gdQ, const void* gdK, const void* gdV, const float* L,
+                         const float* D, const float* alpha, const float* E, void* Kt, void* Vt, void* ws,
+                         int64_t ws_bytes, void* stream) {
+  bool empty;
+  int32_t rc = check_problem(p, &empty);
+  if (rc != BOB_OK) return rc;
+  ColumnPlan c;
+  if ((rc = column_plan(p, true, o, &c)) != BOB_OK || empty) return rc;
+  if ((rc = check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt})) != BOB_OK) return rc;
+  if ((rc = check_workspace(p, c, ws, ws_bytes)) != BOB_OK) return rc;
+  FB_DISPATCH(p, launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt, (hipStream_t)stream, c,
+              (float*)ws);
 }
 
 }  // namespace fb
@@ -125,13 +148,8 @@ int32_t attn_fwd_lse(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, 
 int32_t attn_bwd(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
                  const void* Q, const void* K, const void* V, const void* O, const void* dO,
                  const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, H};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
-  if (rc != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream);
+  return fb::run_bwd(Problem{dtype, B, H, N, d, scale, causal, H}, fb::kUnsplit, Q, K, V, O, dO, L, dQ, dK, dV, D,
+                     nullptr, 0, stream);
 }
 
 int32_t attn_bob_pass1_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale, int32_t causal,
@@ -155,14 +173,8 @@ int32_t attn_bob_pass2_cols(int32_t dtype, int64_t B, int64_t H, int64_t N, int6
                             const void* gdQ, const void* gdK, const void* gdV, const float* L,
                             const float* D, const float* alpha, const float* E, void* Kt, void* Vt,
                             void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, H};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
-  if (rc != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
-              (hipStream_t)stream);
+  return fb::run_pass2(Problem{dtype, B, H, N, d, scale, causal, H}, fb::kUnsplit, Q, K, V, dO, gdQ, gdK, gdV, L,
+                       D, alpha, E, Kt, Vt, nullptr, 0, stream);
 }
 
 // Grouped key/value heads: as above with Hkv key/value heads shared by the H
@@ -182,13 +194,8 @@ int32_t attn_fwd_lse_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64
 int32_t attn_bwd_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
                      int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
                      const float* L, void* dQ, void* dK, void* dV, float* D, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
-  if (rc != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream);
+  return fb::run_bwd(Problem{dtype, B, H, N, d, scale, causal, Hkv}, fb::kUnsplit, Q, K, V, O, dO, L, dQ, dK, dV,
+                     D, nullptr, 0, stream);
 }
 
 int32_t attn_bob_pass1_rows_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
@@ -212,57 +219,57 @@ int32_t attn_bob_pass2_cols_gqa(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
                                 const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                                 const float* L, const float* D, const float* alpha, const float* E, void* Kt,
                                 void* Vt, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
-  if (rc != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
-              (hipStream_t)stream);
+  return fb::run_pass2(Problem{dtype, B, H, N, d, scale, causal, Hkv}, fb::kUnsplit, Q, K, V, dO, gdQ, gdK, gdV,
+                       L, D, alpha, E, Kt, Vt, nullptr, 0, stream);
 }
 
 int64_t bob_pass2_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
-                                  int32_t causal) {
-  return fb::column_ws_bytes(Problem{dtype, B, H, N, d, 1.0f, causal, Hkv}, true);
+                                  int32_t causal, const bob_column_opts* opts) {
+  const Problem p{dtype, B, H, N, d, 1.0f, causal, Hkv};
+  fb::ColumnPlan c;
+  return fb::column_plan(p, true, fb::opts_of(opts), &c) == BOB_OK ? fb::column_workspace_bytes(p, c.parts) : 0;
 }
 
 int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
-                                int32_t causal) {
-  return fb::column_ws_bytes(Problem{dtype, B, H, N, d, 1.0f, causal, Hkv}, false);
+                                int32_t causal, const bob_column_opts* opts) {
+  const Problem p{dtype, B, H, N, d, 1.0f, causal, Hkv};
+  fb::ColumnPlan c;
+  return fb::column_plan(p, false, fb::opts_of(opts), &c) == BOB_OK ? fb::column_workspace_bytes(p, c.parts) : 0;
+}
+
+int32_t bob_column_layout(int32_t kernel, int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                          int32_t causal, const bob_column_opts* opts, bob_column_opts* resolved,
+                          int64_t* workspace_bytes) {
+  if (kernel != BOB_COLUMNS_BWD && kernel != BOB_COLUMNS_PASS2) return BOB_EINVAL;
+  const Problem p{dtype, B, H, N, d, 1.0f, causal, Hkv};
+  fb::ColumnPlan c;
+  const int32_t rc = fb::column_plan(p, kernel == BOB_COLUMNS_PASS2, fb::opts_of(opts), &c);
+  if (rc != BOB_OK) return rc;
+  if (resolved != nullptr) {
+    resolved->parts = c.parts;
+    resolved->wave_sets = c.sets;
+    resolved->flush_tiles = c.flush_tiles > 0 ? c.flush_tiles : -1;
+  }
+  if (workspace_bytes != nullptr) *workspace_bytes = fb::column_workspace_bytes(p, c.parts);
+  return BOB_OK;
 }
 
 int32_t attn_bwd_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d, float scale,
                         int32_t causal, const void* Q, const void* K, const void* V, const void* O, const void* dO,
-                        const float* L, void* dQ, void* dK, void* dV, float* D, void* workspace,
-                        int64_t workspace_bytes, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, O, dO, L, dQ, dK, dV, D});
-  if (rc != BOB_OK) return rc;
-  const int parts = fb::column_parts_of(p, false);
-  if (parts > 1 && (rc = fb::check_workspace(p, parts, workspace, workspace_bytes)) != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_bwd, p, Q, K, V, O, dO, L, dQ, dK, dV, D, (hipStream_t)stream, (float*)workspace,
-              parts);
+                        const float* L, void* dQ, void* dK, void* dV, float* D, const bob_column_opts* opts,
+                        void* workspace, int64_t workspace_bytes, void* stream) {
+  return fb::run_bwd(Problem{dtype, B, H, N, d, scale, causal, Hkv}, fb::opts_of(opts), Q, K, V, O, dO, L, dQ, dK,
+                     dV, D, workspace, workspace_bytes, stream);
 }
 
 int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
                                    float scale, int32_t causal, const void* Q, const void* K, const void* V,
                                    const void* dO, const void* gdQ, const void* gdK, const void* gdV,
                                    const float* L, const float* D, const float* alpha, const float* E, void* Kt,
-                                   void* Vt, void* workspace, int64_t workspace_bytes, void* stream) {
-  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
-  bool empty;
-  int32_t rc = fb::check_problem(p, &empty);
-  if (rc != BOB_OK || empty) return rc;
-  rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt});
-  if (rc != BOB_OK) return rc;
-  const int parts = fb::column_parts_of(p, true);
-  if (parts > 1 && (rc = fb::check_workspace(p, parts, workspace, workspace_bytes)) != BOB_OK) return rc;
-  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt,
-              (hipStream_t)stream, (float*)workspace, parts);
+                                   void* Vt, const bob_column_opts* opts, void* workspace, int64_t workspace_bytes,
+                                   void* stream) {
+  return fb::run_pass2(Problem{dtype, B, H, N, d, scale, causal, Hkv}, fb::opts_of(opts), Q, K, V, dO, gdQ, gdK,
+                       gdV, L, D, alpha, E, Kt, Vt, workspace, workspace_bytes, stream);
 }
 
 int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
@@ -306,18 +313,7 @@ const char* bob_status_string(int32_t status) {
   }
 }
 
-const char* bob_version(void) { return "flashbob-gfx950 0.1"; }
+const char* bob_version(void) { return "flashbob-gfx950 0.2"; }
 
-int32_t bob_set_column_wave_sets(int32_t mode) {
-  if (mode < 0 || mode > 2) return BOB_EINVAL;
-  fb::g_wave_sets.store(mode, std::memory_order_relaxed);
-  return BOB_OK;
-}
-
-int32_t bob_set_column_split(int32_t parts) {
-  if (parts < 0 || parts > fb::kMaxParts) return BOB_EINVAL;
-  fb::g_split.store(parts, std::memory_order_relaxed);
-  return BOB_OK;
-}
 
 }  // extern "C"

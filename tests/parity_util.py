@@ -108,6 +108,50 @@ def check_rows(x, out, w, rows_per_head, seed, slab=64, causal=False, keys=ROW_K
         assert e <= TOL["bf16"], (k, e)
 
 
+def oracle_workers():
+    """Threads for the oracle's slabbed row scalars: the host's cores, at most 16."""
+    import os
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def check_cols(x, out, w, heads, ncols, seed, scalars, causal=False):
+    """Column-owned outputs (Kt, Vt, dK, dV) of the GPU path on `ncols`
+    sampled key rows of each head in `heads` against the oracle's bob_cols.
+
+    A key row sums over every query row, so bob_cols needs L, D, alpha, E of
+    all N rows.  scalars="oracle": the oracle computes them itself for every
+    row (row_scalars), so the check is independent of the GPU.
+    scalars="gpu": the GPU's own L, D, alpha, E are used (a conditional
+    check, for sizes where the oracle cannot form all rows; the caller checks
+    those scalars at sampled rows with check_rows).  Multi-head only."""
+    import time
+    rng = np.random.default_rng(seed)
+    got = {k: [] for k in ("Kt", "Vt", "dK", "dV")}
+    want = {k: [] for k in got}
+    for h in heads:
+        mats = [as_f64(x[n][0, h]) for n in NAMES]
+        t = time.time()
+        if scalars == "oracle":
+            step = max(1, w.N // 8)
+            report = lambda k, n: k % step < 256 and say(f"   head {h}: oracle row scalars {k}/{n} rows")
+            rs = oracle.row_scalars(*mats, w.scale, slab=256, causal=causal, workers=oracle_workers(),
+                                    progress=report)
+        else:
+            rs = {k: as_f64(out[k][0, h]) for k in ("alpha", "E", "L", "D")}
+        cols = np.sort(rng.choice(w.N, size=ncols, replace=False))
+        ref = oracle.bob_cols(*mats, w.scale, cols, rs["alpha"], rs["E"], rs["L"], rs["D"], causal=causal)
+        idx = torch.as_tensor(cols, device=out["Kt"].device)
+        for k in got:
+            got[k].append(as_f64(out[k][0, h].index_select(0, idx)))
+            want[k].append(ref[k])
+        say(f"   head {h}: {ncols} key rows, {scalars} row scalars ({time.time() - t:.1f} s)")
+    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in got}
+    say(f"   sampled-column errs ({scalars} row scalars)", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL["bf16"], (k, e)
+    return errs
+
+
 def check_identities(x, out):
     scal, colsum = global_identities(x, out)
     say("   identities", {k: f"{(a - b) / s:.2e}" for k, (a, b, s) in scal.items()},

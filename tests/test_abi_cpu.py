@@ -189,70 +189,102 @@ def test_binding_checks_group_shapes():
         fb.attn_fwd_lse(q, k2, k2, 0.125)
 
 
-def test_column_wave_set_mode_is_validated(lib):
-    for bad in (-1, 3, 100):
-        assert lib.bob_set_column_wave_sets(bad) == fb.BOB_EINVAL
-    for ok in (1, 2, 0):
-        assert lib.bob_set_column_wave_sets(ok) == fb.BOB_OK
-    with pytest.raises(ValueError):
-        fb.set_column_wave_sets(5)
+def opts(parts=0, wave_sets=0, flush_tiles=0):
+    return ctypes.byref(fb.ColumnOpts(parts, wave_sets, flush_tiles))
 
 
 def call_ws(lib, ws=ALIGNED, nbytes=1 << 40, bad_index=None, dtype=fb.BOB_BF16, B=1, H=4, Hkv=1, N=1000, d=64,
-            causal=1):
+            causal=1, o=None):
     ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(13)]
     if bad_index is not None:
         ptrs[bad_index] = ctypes.c_void_p(0)
     return lib.attn_bob_pass2_cols_gqa_ws(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs,
-                                          ctypes.c_void_p(ws), nbytes, None)
+                                          opts(4) if o is None else o, ctypes.c_void_p(ws), nbytes, None)
 
 
 def call_bwd_ws(lib, ws=ALIGNED, nbytes=1 << 40, bad_index=None, dtype=fb.BOB_BF16, B=1, H=4, Hkv=1, N=1000,
-                d=64, causal=1):
+                d=64, causal=1, o=None):
     ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(10)]
     if bad_index is not None:
         ptrs[bad_index] = ctypes.c_void_p(0)
-    return lib.attn_bwd_gqa_ws(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs, ctypes.c_void_p(ws),
-                               nbytes, None)
+    return lib.attn_bwd_gqa_ws(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs,
+                               opts(4) if o is None else o, ctypes.c_void_p(ws), nbytes, None)
 
 
-def test_column_split_mode_and_workspace(lib):
-    """bob_set_column_split validates its mode; in a forced mode the workspace
-    size is parts x {Kt, Vt} x B*Hkv*N*d fp32 values, and the split call
-    rejects a missing, misaligned or short workspace (and every bad tensor
-    pointer) before any launch."""
-    try:
-        for bad in (-1, 9, 100):
-            assert lib.bob_set_column_split(bad) == fb.BOB_EINVAL
-        assert lib.bob_set_column_split(4) == fb.BOB_OK
-        need = 4 * 2 * 1 * 1 * 1000 * 64 * 4
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == need
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_F32, 2, 4, 2, 100, 32, 0) == 4 * 2 * 2 * 2 * 100 * 32 * 4
-        # empty, invalid and unsupported problems need none (the call reports them)
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 0, 64, 1) == 0
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 3, 1000, 64, 1) == 0
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1) == 0
-        assert call_ws(lib, ws=0) == fb.BOB_EINVAL
-        assert call_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
-        assert call_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
-        for i in range(13):
-            assert call_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
-        assert call_ws(lib, H=4, Hkv=3) == fb.BOB_EINVAL
-        assert call_ws(lib, d=96) == fb.BOB_EUNSUPPORTED
-        assert call_ws(lib, N=0, ws=0) == fb.BOB_OK               # empty: nothing to do
-        # the first backward's split: same size rule and the same checks
-        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == need
-        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1) == 0
-        assert call_bwd_ws(lib, ws=0) == fb.BOB_EINVAL
-        assert call_bwd_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
-        assert call_bwd_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
-        for i in range(10):
-            assert call_bwd_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
-        assert call_bwd_ws(lib, N=0, ws=0) == fb.BOB_OK
-        assert lib.bob_set_column_split(1) == fb.BOB_OK
-        assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == 0
-        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1) == 0
-        with pytest.raises(ValueError):
-            fb.set_column_split(9)
-    finally:
-        lib.bob_set_column_split(0)
+def test_column_split_workspace(lib):
+    """With a forced part count the workspace is parts x {Kt, Vt} x B*Hkv*N*d
+    fp32 values, and the split calls reject a missing, misaligned or short
+    workspace (and every bad tensor pointer) before any launch."""
+    need = 4 * 2 * 1 * 1 * 1000 * 64 * 4
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, opts(4)) == need
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_F32, 2, 4, 2, 100, 32, 0, opts(4)) == 4 * 2 * 2 * 2 * 100 * 32 * 4
+    # empty, invalid and unsupported problems need none (the call reports them)
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 0, 64, 1, opts(4)) == 0
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 3, 1000, 64, 1, opts(4)) == 0
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1, opts(4)) == 0
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, opts(9)) == 0
+    assert call_ws(lib, ws=0) == fb.BOB_EINVAL
+    assert call_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
+    assert call_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
+    for i in range(13):
+        assert call_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
+    assert call_ws(lib, H=4, Hkv=3) == fb.BOB_EINVAL
+    assert call_ws(lib, d=96) == fb.BOB_EUNSUPPORTED
+    assert call_ws(lib, N=0, ws=0) == fb.BOB_OK               # empty: nothing to do
+    # the first backward's split: same size rule and the same checks
+    assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, opts(4)) == need
+    assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 96, 1, opts(4)) == 0
+    assert call_bwd_ws(lib, ws=0) == fb.BOB_EINVAL
+    assert call_bwd_ws(lib, ws=MISALIGNED) == fb.BOB_EINVAL
+    assert call_bwd_ws(lib, nbytes=need - 1) == fb.BOB_EINVAL
+    for i in range(10):
+        assert call_bwd_ws(lib, bad_index=i) == fb.BOB_EINVAL, i
+    assert call_bwd_ws(lib, N=0, ws=0) == fb.BOB_OK
+    # unsplit: no workspace needed, none checked
+    assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, opts(1)) == 0
+    assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, opts(1)) == 0
+
+
+def test_column_opts_are_validated(lib):
+    """Requests out of range are BOB_EINVAL in the calls and the queries;
+    sections where no sectioned form is built are BOB_EUNSUPPORTED."""
+    for bad in (opts(-1), opts(9), opts(0, -1), opts(0, 3), opts(0, 0, -2)):
+        assert call_ws(lib, o=bad) == fb.BOB_EINVAL
+        assert call_bwd_ws(lib, o=bad) == fb.BOB_EINVAL
+        for kernel in (fb.BOB_COLUMNS_BWD, fb.BOB_COLUMNS_PASS2):
+            assert lib.bob_column_layout(kernel, fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, bad, None, None) == fb.BOB_EINVAL
+    assert lib.bob_column_layout(7, fb.BOB_BF16, 1, 4, 1, 1000, 64, 1, None, None, None) == fb.BOB_EINVAL
+    for dt, d in ((fb.BOB_BF16, 256), (fb.BOB_F32, 64)):
+        assert call_ws(lib, dtype=dt, d=d, o=opts(1, 1, 8)) == fb.BOB_EUNSUPPORTED
+        assert call_bwd_ws(lib, dtype=dt, d=d, o=opts(1, 1, 8)) == fb.BOB_EUNSUPPORTED
+        # automatic sections there fall back to one section
+        assert lib.bob_column_layout(fb.BOB_COLUMNS_PASS2, dt, 1, 1, 1, 1 << 20, d, 0, opts(1), None, None) == 0
+
+
+def layout(lib, kernel, o, dtype=fb.BOB_BF16, B=1, H=4, Hkv=1, N=1000, d=64, causal=1):
+    got = fb.ColumnOpts()
+    nbytes = ctypes.c_int64(-1)
+    rc = lib.bob_column_layout(kernel, dtype, B, H, Hkv, N, d, causal, o, ctypes.byref(got), ctypes.byref(nbytes))
+    assert rc == fb.BOB_OK
+    return (got.parts, got.wave_sets, got.flush_tiles), nbytes.value
+
+
+def test_column_layout_resolves_requests(lib):
+    """Forced requests come back as given; a split runs one wave set; a long
+    stream gets sections of 1024 tiles when sections are automatic (bf16
+    d <= 128), and asking for one section (-1) keeps a single chain."""
+    for kernel in (fb.BOB_COLUMNS_BWD, fb.BOB_COLUMNS_PASS2):
+        assert layout(lib, kernel, opts(3, 2, 5)) == ((3, 1, 5), 3 * 2 * 1000 * 64 * 4)
+        assert layout(lib, kernel, opts(1, 1, 2)) == ((1, 1, 2), 0)
+        assert layout(lib, kernel, opts(1, 2, -1)) == ((1, 2, -1), 0)
+        # B1 H1 N = 2^20, d = 64: 32768 streamed tiles in one chain -> sections
+        for d in (32, 64, 128):
+            assert layout(lib, kernel, opts(1, 1), H=1, N=1 << 20, d=d, causal=0) == ((1, 1, 1024), 0)
+            assert layout(lib, kernel, opts(1, 1, -1), H=1, N=1 << 20, d=d, causal=0) == ((1, 1, -1), 0)
+            # 8192 tiles stay in one chain; split in 8 parts the chain is short again
+            assert layout(lib, kernel, opts(1, 1), H=1, N=1 << 18, d=d, causal=0) == ((1, 1, -1), 0)
+            assert layout(lib, kernel, opts(8, 1), H=1, N=1 << 20, d=d, causal=0)[0] == (8, 1, -1)
+        # grouped heads lengthen the stream: 16 query heads x 1024 tiles
+        assert layout(lib, kernel, opts(1, 1), H=16, Hkv=1, N=32768, d=64, causal=0)[0] == (1, 1, 1024)
+    # the empty problem has the trivial layout
+    assert layout(lib, fb.BOB_COLUMNS_PASS2, None, N=0) == ((1, 1, -1), 0)

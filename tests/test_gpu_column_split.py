@@ -1,13 +1,15 @@
 """GPU parity of the column kernels (the first backward's dK, dV and Pass
 2's Kt, Vt) with each key/value column block split over several workgroups
 (attn_bwd_gqa_ws, attn_bob_pass2_cols_gqa_ws; forced with
-bob_set_column_split):
+bob_column_opts.parts):
 every split is checked against the float64 oracle on multi-head and grouped
 problems, dense and causal, including splits into more parts than a block
 has (query head, query tile) iterations, so that some parts stream nothing
 and store zeros; the row-owned outputs must not depend on the split, and dK,
 dV, Kt, Vt must agree with the unsplit kernels to the rounding of the fp32
 sums."""
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -42,8 +44,13 @@ def case_id(c):
 def fb():
     import paper_2609_24089_amd as m
     m.load_library()
-    yield m
-    m.set_column_split(0)
+    return m
+
+
+def ws_bytes(fb, pass2, code, B, H, Hkv, N, d, causal, columns=None):
+    lib = fb.load_library()
+    q = lib.bob_pass2_workspace_bytes if pass2 else lib.bob_bwd_workspace_bytes
+    return q(code, B, H, Hkv, N, d, int(causal), None if columns is None else ctypes.byref(columns))
 
 
 @pytest.mark.parametrize("case", CASES, ids=case_id)
@@ -54,19 +61,18 @@ def test_split_matches_oracle_and_unsplit(fb, case):
     scale = 1.0 / np.sqrt(d)
     ref = oracle.bob_gqa(*[as_f64(x[n]) for n in NAMES], scale, causal=causal)
     xd = {k: v.cuda() for k, v in x.items()}
-    lib = fb.load_library()
     code = fb.BOB_BF16 if dt == "bf16" else fb.BOB_F32
-    fb.set_column_split(1)
-    assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == 0
-    assert lib.bob_bwd_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == 0
-    base = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
+    one = fb.ColumnOpts(1, 1, 0)
+    assert ws_bytes(fb, True, code, B, H, Hkv, N, d, causal, one) == 0
+    assert ws_bytes(fb, False, code, B, H, Hkv, N, d, causal, one) == 0
+    base = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal, columns=one)
     torch.cuda.synchronize()
     for parts in (2, 3, 8):
-        fb.set_column_split(parts)
+        cols = fb.ColumnOpts(parts, 0, 0)
         want = parts * 2 * B * Hkv * N * d * 4
-        assert lib.bob_pass2_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == want
-        assert lib.bob_bwd_workspace_bytes(code, B, H, Hkv, N, d, int(causal)) == want
-        out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
+        assert ws_bytes(fb, True, code, B, H, Hkv, N, d, causal, cols) == want
+        assert ws_bytes(fb, False, code, B, H, Hkv, N, d, causal, cols) == want
+        out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal, columns=cols)
         torch.cuda.synchronize()
         errs = {k: nrel(as_f64(out[k]), ref[k]) for k in OUTS}
         say(f"   parts {parts} errs", {k: f"{v:.2e}" for k, v in errs.items()})
@@ -91,28 +97,27 @@ def test_split_on_a_side_stream(fb):
     O, L = fb.attn_fwd_lse(Q, K, V, scale, True)
     dQ, dK, dV, D = fb.attn_bwd(Q, K, V, O, dO, L, scale, True)
     Qt, dOt, al, E = fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, scale, True, dQ=dQ)
-    fb.set_column_split(4)
-    ref = fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True)
+    cols = fb.ColumnOpts(4, 0, 0)
+    ref = fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True, columns=cols)
     torch.cuda.synchronize()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     outs = []
     for _ in range(3):
-        outs.append(fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True, stream=side))
+        outs.append(fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, True, stream=side,
+                                           columns=cols))
     side.synchronize()
     for kt, vt in outs:
         assert torch.equal(kt, ref[0]) and torch.equal(vt, ref[1])
 
 
 def test_automatic_choice(fb):
-    """Mode 0 splits a causal grid up to about 8 jobs per CU (at most 8
+    """Automatic parts split a causal grid up to about 8 jobs per CU (at most 8
     parts); Pass 2 splits a dense grid only when it has fewer workgroups than
     CUs, the first backward to about 8 jobs per CU as well; blocks of fewer
     than 1024 streamed iterations and the multi-head workloads stay
     unsplit; the automatic result equals the forced one bit for bit."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    lib = fb.load_library()
-    fb.set_column_split(0)
     N, d = 16384, 128
     grid = lambda Hkv: Hkv * (N // 64)          # bf16 d = 128 Pass 2: 64 key rows per workgroup
     expect = lambda g, causal: (min(8, -(-8 * cus // g)) if causal else
@@ -121,19 +126,19 @@ def test_automatic_choice(fb):
         parts = expect(grid(Hkv), causal)
         parts = parts if parts >= 2 else 1
         want = 0 if parts == 1 else parts * 2 * Hkv * N * d * 4
-        got = lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal)
+        got = ws_bytes(fb, True, fb.BOB_BF16, 1, 16, Hkv, N, d, causal)
         say(f"[column split] auto Hkv={Hkv} causal={causal} CUs {cus}: {got} bytes (parts {parts})")
         assert got == want, (Hkv, causal, got, want)
         # the first backward's column kernel also owns 64 key rows per
         # workgroup here, and is split to about 8 jobs per CU under either mask
         pb = min(8, -(-8 * cus // grid(Hkv)))
         want_b = 0 if pb < 2 else pb * 2 * Hkv * N * d * 4
-        assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 1, 16, Hkv, N, d, causal) == want_b, (Hkv, causal)
+        assert ws_bytes(fb, False, fb.BOB_BF16, 1, 16, Hkv, N, d, causal) == want_b, (Hkv, causal)
     # short blocks (fewer than 1024 streamed iterations) are never split
     for Hkv, n in ((12, 4096), (12, 2048), (1, 500)):
         for causal in (0, 1):
-            assert lib.bob_pass2_workspace_bytes(fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
-            assert lib.bob_bwd_workspace_bytes(fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
+            assert ws_bytes(fb, True, fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
+            assert ws_bytes(fb, False, fb.BOB_BF16, 4, 12 if Hkv == 12 else 4, Hkv, n, 64, causal) == 0
     # a causal multi-query problem with 16 x 64 = 1024 iterations per block:
     # automatic equals the forced part count
     B, H, Hkv, n = 1, 16, 1, 2048
@@ -141,8 +146,7 @@ def test_automatic_choice(fb):
     parts = min(8, -(-8 * cus // g))
     xd = {k: v.cuda() for k, v in make_gqa_inputs(B, H, Hkv, n, 128, "bf16", 179).items()}
     auto = fb.bob(*[xd[k] for k in NAMES], 0.1, causal=True)
-    fb.set_column_split(parts)
-    forced = fb.bob(*[xd[k] for k in NAMES], 0.1, causal=True)
+    forced = fb.bob(*[xd[k] for k in NAMES], 0.1, causal=True, columns=fb.ColumnOpts(parts, 0, 0))
     torch.cuda.synchronize()
     for k in OUTS:
         assert torch.equal(auto[k], forced[k]), k

@@ -1,7 +1,7 @@
 """GPU parity of the column-owned kernels (the dK, dV half of the first
 backward, and Pass 2) in both of their workgroup forms: one wave set per
 column block, and two wave sets that take alternate streamed tiles and add
-their fp32 partial sums at the end (bob_set_column_wave_sets).  Each form is
+their fp32 partial sums at the end (bob_column_opts.wave_sets).  Each form is
 checked against the float64 oracle on multi-head and grouped problems, dense
 and causal, with iteration counts that are odd (the second set's last
 iteration has no tile) or 1 (the second set has none at all); the row-owned
@@ -42,15 +42,12 @@ def case_id(c):
 def fb():
     import paper_2609_24089_amd as m
     m.load_library()
-    m.set_column_split(1)   # Pass 2 would otherwise split these small grids over workgroups
-    yield m
-    m.set_column_wave_sets(0)
-    m.set_column_split(0)
+    return m
 
 
 def run(fb, xd, scale, causal, mode):
-    fb.set_column_wave_sets(mode)
-    out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal)
+    # unsplit (Pass 2 would otherwise split these small grids over workgroups)
+    out = fb.bob(*[xd[n] for n in NAMES], scale, causal=causal, columns=fb.ColumnOpts(1, mode, 0))
     torch.cuda.synchronize()
     return out
 
