@@ -33,9 +33,12 @@
  *  pointers  device pointers owned by the caller, 16-byte aligned, on the
  *          current HIP device (the kernels run there).  The library
  *          allocates no memory (the *_ws calls take their workspace from
- *          the caller) and keeps no state: every choice it makes depends
- *          only on the arguments and on the current device's compute-unit
- *          count, so the entry points are thread-safe.
+ *          the caller) and keeps no state apart from the device address of
+ *          the static scratch buffer of attn_bob_pass2_cols_gqa_noalloc:
+ *          every choice it makes depends only on the arguments and on the
+ *          current device's compute-unit count, so the entry points are
+ *          thread-safe (two _noalloc calls that overlap on one device race
+ *          on its scratch, see there).
  *          Outputs must not alias inputs.
  *  stream  a hipStream_t of the current device passed as void* (NULL = the
  *          default stream).  Work
@@ -68,7 +71,8 @@ typedef enum {
   BOB_OK = 0,
   BOB_EINVAL = 1,
   BOB_EUNSUPPORTED = 2,
-  BOB_ELAUNCH = 3
+  BOB_ELAUNCH = 3,
+  BOB_ESCRATCH = 4
 } bob_status;
 
 /* Layout of a column-owned kernel: the first backward's dK, dV kernel or
@@ -230,6 +234,39 @@ int64_t bob_bwd_workspace_bytes(int32_t dtype, int64_t B, int64_t H, int64_t Hkv
 int32_t bob_column_layout(int32_t kernel, int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
                           int32_t causal, const bob_column_opts* opts, bob_column_opts* resolved,
                           int64_t* workspace_bytes);
+
+/* Pass 2 for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): as
+ * attn_bob_pass2_cols_gqa_ws, but a split layout keeps its fp32 partial sums
+ * in a scratch buffer the library holds in static device memory instead of
+ * a caller's workspace.  The call itself allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the caller passes inputs and
+ * outputs as usual.
+ *  scratch  bob_scratch_bytes() (64 MiB) per device, part of the library's
+ *          code object, held by every device the library runs on until the
+ *          process ends.  A split needs parts x 2 x B x Hkv x N x d x 4 bytes
+ *          of it.  With parts automatic (opts NULL or opts->parts == 0) the
+ *          call uses the largest automatic part count that fits, or runs
+ *          unsplit; a forced opts->parts whose split does not fit gives
+ *          BOB_ESCRATCH before any launch.
+ *  races   every call on one device shares that device's scratch, which
+ *          keeps the last call's contents (a split writes every element it
+ *          later reads, so nothing needs clearing).  Two calls that overlap
+ *          on one device (different streams, or different host threads)
+ *          race on it and give wrong results: order them on one stream or
+ *          with events.  Calls that do not split do not touch it.
+ * Results equal those of attn_bob_pass2_cols_gqa_ws with the same resolved
+ * layout (bob_column_layout with the same part count), bit for bit.
+ * Errors as attn_bob_pass2_cols_gqa_ws, plus BOB_ESCRATCH, and BOB_ELAUNCH
+ * if the scratch buffer's device address cannot be read. */
+int32_t attn_bob_pass2_cols_gqa_noalloc(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                        float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                        const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                        const float* L, const float* D, const float* alpha, const float* E,
+                                        void* Kt, void* Vt, const bob_column_opts* opts, void* stream);
+
+/* Bytes of the static scratch buffer attn_bob_pass2_cols_gqa_noalloc uses. */
+int64_t bob_scratch_bytes(void);
 
 /* Three-pass control schedule (App. "Three-pass versus two-pass" and the
  * three-pass overlay of App. "Dependency graphs"): the schedule that the

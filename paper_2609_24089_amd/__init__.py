@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libflashbob.so")
 
 BOB_F32 = 0
 BOB_BF16 = 1
-BOB_OK, BOB_EINVAL, BOB_EUNSUPPORTED, BOB_ELAUNCH = 0, 1, 2, 3
+BOB_OK, BOB_EINVAL, BOB_EUNSUPPORTED, BOB_ELAUNCH, BOB_ESCRATCH = 0, 1, 2, 3, 4
 BOB_COLUMNS_BWD, BOB_COLUMNS_PASS2 = 0, 1
 
 _lib = None
@@ -80,6 +80,10 @@ def load_library():
     lib.attn_bob_pass2_cols_gqa_ws.restype = i32
     lib.attn_bwd_gqa_ws.argtypes = common_gqa + [vp] * 10 + [opts_p, vp, i64] + [vp]
     lib.attn_bwd_gqa_ws.restype = i32
+    lib.attn_bob_pass2_cols_gqa_noalloc.argtypes = common_gqa + [vp] * 13 + [opts_p] + [vp]
+    lib.attn_bob_pass2_cols_gqa_noalloc.restype = i32
+    lib.bob_scratch_bytes.argtypes = []
+    lib.bob_scratch_bytes.restype = i64
     _lib = lib
     return lib
 
@@ -286,6 +290,26 @@ def attn_bob_pass2_cols(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causa
     ws, nbytes = _column_workspace(lib.bob_pass2_workspace_bytes, code, B, H, Hkv, N, d, c, columns, Q, stream)
     _call(Q, lib.attn_bob_pass2_cols_gqa_ws, code, B, H, Hkv, N, d, float(scale), c, *ptrs, _opts(columns),
           None if ws is None else _p(ws), nbytes, st)
+    return Kt, Vt
+
+
+def attn_bob_pass2_cols_noalloc(Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, scale, causal=False, out=None,
+                                stream=None, columns=None):
+    """Pass 2 through attn_bob_pass2_cols_gqa_noalloc: a split layout keeps its
+    partial sums in the library's static scratch buffer, so the call allocates
+    no device memory (pass `out` to allocate nothing here either).  Calls that
+    overlap on one device race on that buffer.  Returns (Kt, Vt)."""
+    B, H, Hkv, N, d = _check_groups((Q, dO, gdQ), (K, V, gdK, gdV))
+    _check_rows(Q.shape, L, D, alpha, E)
+    if out is None:
+        out = (torch.empty_like(K), torch.empty_like(K))
+    Kt, Vt = out
+    _check_mats(K, Kt, Vt)
+    lib = load_library()
+    ptrs = (_p(Q), _p(K), _p(V), _p(dO), _p(gdQ), _p(gdK), _p(gdV), _p(L), _p(D), _p(alpha), _p(E),
+            _p(Kt), _p(Vt))
+    _call(Q, lib.attn_bob_pass2_cols_gqa_noalloc, _dtype_code(Q), B, H, Hkv, N, d, float(scale),
+          int(bool(causal)), *ptrs, _opts(columns), _stream(stream, Q))
     return Kt, Vt
 
 

@@ -1,5 +1,6 @@
 // C ABI of libflashbob.so: argument validation and kernel dispatch.
 // The entry points are declared (and documented) in include/flashbob.h.
+#include <atomic>
 #include <type_traits>
 
 #include "fb_launch.h"
@@ -126,6 +127,45 @@ static int32_t run_pass2(const Problem& p, const ColumnOpts& o, const void* Q, c
   if ((rc = check_workspace(p, c, ws, ws_bytes)) != BOB_OK) return rc;
   FB_DISPATCH(p, launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt, (hipStream_t)stream, c,
               (float*)ws);
+}
+
+// Scratch of attn_bob_pass2_cols_gqa_noalloc, for callers that cannot
+// allocate: the fp32 partial sums of a split Pass 2 (the *_ws workspace).
+// Each device the library runs on holds its own copy until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device
+// memory: kernels get the address hipGetSymbolAddress returns for the
+// current device, read once per device and kept in scratch_dev.
+constexpr int64_t kScratchBytes = int64_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static std::atomic<void*> scratch_dev[kMaxDevices];
+
+// Device address of `scratch` on the current device, or nullptr if it
+// cannot be read.
+static void* scratch_ptr() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* ptr = scratch_dev[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+    scratch_dev[dev].store(ptr, std::memory_order_release);   // the same address on every call
+  }
+  return ptr;
+}
+
+// The layout of Pass 2 with its workspace in `scratch`: as requested; when
+// the part count is automatic and its workspace would not fit, the largest
+// part count that fits (or none).  A forced part count that does not fit
+// gives BOB_ESCRATCH.
+static int32_t noalloc_plan(const Problem& p, const ColumnOpts& o, ColumnPlan* c) {
+  int32_t rc = column_plan(p, true, o, c);
+  if (rc != BOB_OK || column_workspace_bytes(p, c->parts) <= kScratchBytes) return rc;
+  if (o.parts != 0) return BOB_ESCRATCH;
+  const int64_t per_part = column_workspace_bytes(p, 2) / 2;
+  const int fit = (int)std::min<int64_t>(kScratchBytes / per_part, kMaxParts);
+  ColumnOpts capped = o;
+  capped.parts = fit >= 2 ? std::min(fit, c->parts) : 1;
+  return column_plan(p, true, capped, c);
 }
 
 }  // namespace fb
@@ -272,6 +312,26 @@ int32_t attn_bob_pass2_cols_gqa_ws(int32_t dtype, int64_t B, int64_t H, int64_t 
                        gdV, L, D, alpha, E, Kt, Vt, workspace, workspace_bytes, stream);
 }
 
+int32_t attn_bob_pass2_cols_gqa_noalloc(int32_t dtype, int64_t B, int64_t H, int64_t Hkv, int64_t N, int64_t d,
+                                        float scale, int32_t causal, const void* Q, const void* K, const void* V,
+                                        const void* dO, const void* gdQ, const void* gdK, const void* gdV,
+                                        const float* L, const float* D, const float* alpha, const float* E,
+                                        void* Kt, void* Vt, const bob_column_opts* opts, void* stream) {
+  const Problem p{dtype, B, H, N, d, scale, causal, Hkv};
+  bool empty;
+  int32_t rc = fb::check_problem(p, &empty);
+  if (rc != BOB_OK) return rc;
+  fb::ColumnPlan c;
+  if ((rc = fb::noalloc_plan(p, fb::opts_of(opts), &c)) != BOB_OK || empty) return rc;
+  if ((rc = fb::check_ptrs({Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt})) != BOB_OK) return rc;
+  float* ws = nullptr;
+  if (c.parts > 1 && (ws = (float*)fb::scratch_ptr()) == nullptr) return BOB_ELAUNCH;
+  FB_DISPATCH(p, fb::launch_pass2, p, Q, K, V, dO, gdQ, gdK, gdV, L, D, alpha, E, Kt, Vt, (hipStream_t)stream, c,
+              ws);
+}
+
+int64_t bob_scratch_bytes(void) { return fb::kScratchBytes; }
+
 int32_t attn_bob3_alpha_rows(int32_t dtype, int64_t B, int64_t H, int64_t N, int64_t d, float scale,
                              int32_t causal, const void* Q, const void* K, const void* gdQ, const void* gdK,
                              const float* L, float* alpha, void* stream) {
@@ -309,6 +369,9 @@ const char* bob_status_string(int32_t status) {
     case BOB_EUNSUPPORTED:
       return "BOB_EUNSUPPORTED: (dtype, head dim) not built; bf16 d = 32, 64, 128, 256; fp32 d = 32, 64, 128";
     case BOB_ELAUNCH: return "BOB_ELAUNCH: HIP kernel launch failed";
+    case BOB_ESCRATCH:
+      return "BOB_ESCRATCH: the requested layout needs more scratch than the library's static buffer "
+             "(bob_scratch_bytes())";
     default: return "unknown bob_status";
   }
 }

@@ -46,7 +46,7 @@ def test_supported_and_strings(lib):
         assert lib.bob_supported(fb.BOB_F32, d) == 1, d
     assert lib.bob_supported(fb.BOB_F32, 256) == 0
     assert lib.bob_supported(fb.BOB_BF16, 96) == 0 and lib.bob_supported(7, 64) == 0
-    for rc in range(4):
+    for rc in range(5):
         assert lib.bob_status_string(rc).decode().startswith("BOB_")
     assert lib.bob_status_string(99).decode() == "unknown bob_status"
     assert lib.bob_version().decode().startswith("flashbob")
@@ -288,3 +288,32 @@ def test_column_layout_resolves_requests(lib):
         assert layout(lib, kernel, opts(1, 1), H=16, Hkv=1, N=32768, d=64, causal=0)[0] == (1, 1, 1024)
     # the empty problem has the trivial layout
     assert layout(lib, fb.BOB_COLUMNS_PASS2, None, N=0) == ((1, 1, -1), 0)
+
+
+def call_noalloc(lib, o=None, bad_index=None, dtype=fb.BOB_BF16, B=1, H=16, Hkv=1, N=16384, d=128, causal=1):
+    ptrs = [ctypes.c_void_p(ALIGNED) for _ in range(13)]
+    if bad_index is not None:
+        ptrs[bad_index] = ctypes.c_void_p(0)
+    return lib.attn_bob_pass2_cols_gqa_noalloc(dtype, B, H, Hkv, N, d, ctypes.c_float(0.125), causal, *ptrs, o,
+                                               None)
+
+
+def test_noalloc_rejects_before_launching(lib):
+    """The allocation-free Pass 2 checks its problem, request and pointers
+    like the *_ws call, and refuses a forced split whose partial sums would
+    not fit its static scratch (BOB_ESCRATCH), all before any HIP call."""
+    cap = lib.bob_scratch_bytes()
+    assert cap == 64 << 20
+    # B1 Hkv1 N16384 d128: 16 MiB of fp32 per {Kt, Vt} part pair x parts
+    per_part = 2 * 16384 * 128 * 4
+    assert 4 * per_part <= cap < 5 * per_part
+    assert call_noalloc(lib, opts(5)) == fb.BOB_ESCRATCH
+    assert call_noalloc(lib, opts(8)) == fb.BOB_ESCRATCH
+    assert lib.bob_status_string(fb.BOB_ESCRATCH).decode().startswith("BOB_ESCRATCH")
+    for bad in (opts(-1), opts(0, 3), opts(0, 0, -2)):
+        assert call_noalloc(lib, bad) == fb.BOB_EINVAL
+    for i in range(13):
+        assert call_noalloc(lib, opts(1), bad_index=i) == fb.BOB_EINVAL, i
+    assert call_noalloc(lib, opts(1), d=96) == fb.BOB_EUNSUPPORTED
+    assert call_noalloc(lib, opts(1), H=4, Hkv=3) == fb.BOB_EINVAL
+    assert call_noalloc(lib, None, N=0) == fb.BOB_OK
