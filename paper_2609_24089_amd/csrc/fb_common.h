@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace fb {
 
 typedef __bf16 bf16;
@@ -308,45 +310,72 @@ constexpr int tile_loads() {
   return NTENS * Geo<T, D>::kBlocks / NW;
 }
 
-// w is the wave's index among the NW waves that share the copy.
+// The copy of NTENS streamed tiles by one of the NW waves that share it (w
+// its index among them; TileCopy is built once, before the tile loop), with
+// buffer_load ... lds.  Per tile and tensor the wave builds, in scalar
+// registers, a buffer resource whose base is the tile's first row and whose
+// size ends at row N; each lane's 32-bit byte offset into the tile (its
+// chunk's row and column) is the same for every tile.  Issuing a tile
+// therefore costs no vector address arithmetic, and rows at or past N read
+// as zeros by the buffer's range check (finite data that every kernel masks
+// out).
 template <typename T, int D, int NW, int NTENS>
-__device__ __forceinline__ void issue_tiles(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N,
-                                            int w = wave_id()) {
+struct TileCopy {
   using G = Geo<T, D>;
-  constexpr int kBlockElems = 1024 / (int)sizeof(T);
-  const int l = lane_id();
-  auto one = [&](const T* base, int t, int b) {
-    int r, c;
-    G::slot_source(b * 64 + l, r, c);
-    const int row = min(s0 + r, N - 1);
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(base + (int64_t)row * D + c * G::kEPC),
-        (__attribute__((address_space(3))) void*)(dst + t * G::kTileElems + b * kBlockElems), 16, 0, 0);
-  };
-  if constexpr (G::kBlocks % NW == 0) {
-    // every wave takes the same block positions of every tensor
+  static constexpr int kBlockElems = 1024 / (int)sizeof(T);
+  static constexpr bool kAllTensors = G::kBlocks % NW == 0;   // else kWPB waves share a block position
+  static constexpr int kWPB = kAllTensors ? 1 : NW / G::kBlocks;
+  static constexpr int kPos = kAllTensors ? G::kBlocks / NW : 1;   // block positions this wave copies
+  static constexpr int kRowBytes = D * (int)sizeof(T);
+  static_assert(kAllTensors || (NW % G::kBlocks == 0 && NTENS % kWPB == 0), "tile blocks per wave");
+  int w;                       // wave-uniform
+  uint32_t off[kPos];          // per-lane byte offset of the lane's chunk from the tile's first row
+
+  __device__ __forceinline__ explicit TileCopy(int wave) {
+    w = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
-    for (int bi = 0; bi < G::kBlocks / NW; ++bi)
-#pragma unroll
-      for (int t = 0; t < NTENS; ++t) one(src[t], t, w + bi * NW);
-  } else {
-    // more waves than blocks per tensor: kWPB waves share a block position
-    // and split the tensors between them (tensor index chosen by selects,
-    // not by indexing the pointer array, which would go through scratch)
-    constexpr int kWPB = NW / G::kBlocks;
-    static_assert(NW % G::kBlocks == 0 && NTENS % kWPB == 0, "tile blocks per wave");
-    const int b = w % G::kBlocks, t0 = w / G::kBlocks;
-#pragma unroll
-    for (int i = 0; i < NTENS / kWPB; ++i) {
-      const int t = t0 + i * kWPB;
-      const T* base = src[0];
-#pragma unroll
-      for (int u = 1; u < NTENS; ++u)
-        if (t == u) base = src[u];
-      one(base, t, b);
+    for (int i = 0; i < kPos; ++i) {
+      int r, c;
+      G::slot_source(block(i) * 64 + lane_id(), r, c);
+      off[i] = (uint32_t)(r * kRowBytes + c * 16);
     }
   }
-}
+  __device__ __forceinline__ int block(int i) const { return kAllTensors ? w + i * NW : w % G::kBlocks; }
+
+  __device__ __forceinline__ void issue(const T* const (&src)[NTENS], T FB_LDS* dst, int s0, int N) const {
+    // bytes from row s0 to the end of the tile or of the matrix (< 2^31)
+    const int bytes = min(N - s0, kBS) * kRowBytes;
+    auto one = [&](const T* base, int t, int i) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource type exists for the device target only
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(base + (int64_t)s0 * D), (short)0, bytes, 0x00020000);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void*)(dst + t * G::kTileElems + block(i) * kBlockElems), 16,
+          off[i], 0, 0, 0);
+#endif
+    };
+    if constexpr (kAllTensors) {
+      // every wave takes the same block positions of every tensor
+#pragma unroll
+      for (int i = 0; i < kPos; ++i)
+#pragma unroll
+        for (int t = 0; t < NTENS; ++t) one(src[t], t, i);
+    } else {
+      // tensor index chosen by selects, not by indexing the pointer array
+      // (which would go through scratch)
+      const int t0 = w / G::kBlocks;
+#pragma unroll
+      for (int k = 0; k < NTENS / kWPB; ++k) {
+        const int t = t0 + k * kWPB;
+        const T* base = src[0];
+#pragma unroll
+        for (int u = 1; u < NTENS; ++u)
+          if (t == u) base = src[u];
+        one(base, t, 0);
+      }
+    }
+  }
+};
 
 // Wait until at most N vector-memory loads of this wave are outstanding
 // (loads complete in issue order for this count).
@@ -381,7 +410,11 @@ __device__ __forceinline__ void mask_tile(floatx4 (&x)[2][M], int s0, int t0, in
 // stream through an NSTAGE-deep LDS ring.  issue(tile, stage) starts the
 // asynchronous copies of one tile (row scalars first, then the matrices, so
 // that at most LT loads per wave are younger than the previous tile's);
-// body(tile, stage) consumes a resident tile.  One barrier per tile.
+// body(tile, stage) consumes a resident tile.  One barrier per tile.  The
+// loop is unrolled by NSTAGE, so every ring-stage index the two callbacks
+// see is a compile-time constant: LDS addresses become loop-invariant
+// registers plus immediate offsets, and the copy's LDS destination a
+// constant.
 template <int NSTAGE, int LT, class Issue, class Body>
 __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& issue, Body&& body) {
   static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
@@ -391,12 +424,13 @@ __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& is
     if (st < n) issue(it_begin + st, st);
   wait_vm<0>();
   __syncthreads();
-  int cur = 0;  // stage holding the current tile
-  for (int k = 0; k < n; ++k) {
+  // iteration k consumes stage k % NSTAGE and refills stage (k - 1) % NSTAGE
+  auto step = [&](int k, auto cur) {
+    constexpr int kCur = decltype(cur)::value;
+    constexpr int kNext = kCur == 0 ? NSTAGE - 1 : kCur - 1;
     const int nx = k + NSTAGE - 1;  // tile fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
-    if (nx < n) issue(it_begin + nx, nxs);
-    body(it_begin + k, cur);
+    if (nx < n) issue(it_begin + nx, kNext);
+    body(it_begin + k, kCur);
     // the next tile must have landed; with three stages the one after it may
     // still be in flight
     if (NSTAGE == 3 && nx < n)
@@ -404,7 +438,12 @@ __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& is
     else
       wait_vm<0>();
     __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
+  };
+  for (int k = 0; k < n; k += NSTAGE) {
+    step(k, std::integral_constant<int, 0>{});
+    if (k + 1 < n) step(k + 1, std::integral_constant<int, 1>{});
+    if constexpr (NSTAGE == 3)
+      if (k + 2 < n) step(k + 2, std::integral_constant<int, 2>{});
   }
 }
 // stream_loop for a kernel that transforms the streamed row scalars once per
@@ -417,46 +456,43 @@ __device__ __forceinline__ void stream_loop(int it_begin, int it_end, Issue&& is
 // tile t-2 used, and the barrier at the end of the iteration publishes them.
 // issue_m(tile, matrix stage) issues LT loads per wave; issue_s(tile, scalar
 // stage) and prep(tile, scalar stage, transformed slot) run on the owner only;
-// body(tile, matrix stage, transformed slot, prep_next).
+// body(tile, matrix stage, transformed slot, prep_next).  Two stages: the
+// loop is unrolled by two, so every stage and slot index is a compile-time
+// constant (as in stream_loop).
 template <int NSTAGE, int LT, int LS, class IssueS, class IssueM, class Prep, class Body>
 __device__ __forceinline__ void stream_loop_rs(int it_begin, int it_end, bool owner, IssueS&& issue_s,
                                                IssueM&& issue_m, Prep&& prep, Body&& body) {
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "pipeline depth");
+  static_assert(NSTAGE == 2, "the column kernels run a two-stage ring");
   const int n = it_end - it_begin;
   if (owner && n > 0) issue_s(it_begin, 0);
-#pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < n) {
-      if (owner && st + 1 < n) issue_s(it_begin + st + 1, st + 1);
-      issue_m(it_begin + st, st);
-    }
+  if (n > 0) {
+    if (owner && 1 < n) issue_s(it_begin + 1, 1);
+    issue_m(it_begin, 0);
+  }
   wait_vm<0>();
   if (owner && n > 0) prep(it_begin, 0, 0);
   __syncthreads();
-  int cur = 0;  // matrix stage of the current tile
-  for (int k = 0; k < n; ++k) {
-    const int nx = k + NSTAGE - 1;  // matrices fetched during this iteration
-    const int nxs = (cur == 0) ? NSTAGE - 1 : cur - 1;
+  // iteration k: matrices in stage k % 2 (the next tile's go to the other
+  // stage), raw scalars of tile k + 2 into stage k % 2, transformed scalars of
+  // tile k in slot k % 2
+  auto step = [&](int k, auto cur) {
+    constexpr int kCur = decltype(cur)::value, kOther = 1 - kCur;
+    const int nx = k + 1;
     if (nx < n) {
-      if (owner && nx + 1 < n) issue_s(it_begin + nx + 1, (nx + 1) % NSTAGE);
-      issue_m(it_begin + nx, nxs);
+      if (owner && nx + 1 < n) issue_s(it_begin + nx + 1, kCur);
+      issue_m(it_begin + nx, kOther);
     }
-    body(it_begin + k, cur, k & 1, [&]() {
-      if (owner && k + 1 < n) prep(it_begin + k + 1, (k + 1) % NSTAGE, (k + 1) & 1);
+    body(it_begin + k, kCur, kCur, [&]() {
+      if (owner && k + 1 < n) prep(it_begin + k + 1, kOther, kOther);
     });
     // the next tile's matrices (and, on the owner, the scalars of the tile
-    // after) must have landed; with three stages this iteration's copies may
-    // still be in flight
-    if (NSTAGE == 3 && nx < n) {
-      if (owner && nx + 1 < n)
-        wait_vm<LT + LS>();
-      else
-        wait_vm<LT>();
-    } else {
-      wait_vm<0>();
-    }
+    // after) must have landed
+    wait_vm<0>();
     __syncthreads();
-    cur = (cur + 1 == NSTAGE) ? 0 : cur + 1;
+  };
+  for (int k = 0; k < n; k += 2) {
+    step(k, std::integral_constant<int, 0>{});
+    if (k + 1 < n) step(k + 1, std::integral_constant<int, 1>{});
   }
 }
 

@@ -108,9 +108,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
   const T* const src[2] = {K + kvoff, V + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  const TileCopy<T, D, NW, 2> copy(wave_id());
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       0, it_end,
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) { copy.issue(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
         const int s0 = it * kBS;
         const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
@@ -220,9 +221,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
   const T* const src[2] = {K + kvoff, V + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  const TileCopy<T, D, NW, 2> copy(wave_id());
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       0, it_end,
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) { copy.issue(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
         const int s0 = it * kBS;
         const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
@@ -353,6 +355,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   const int it_begin = causal ? (rb * BC) / kBS : 0;
   const int nTh = nT - it_begin;
   const StreamSplit<kGQA, KS, kParts> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp, part, nparts};
+  const TileCopy<T, D, NW, 2> copy(wl);
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 2>(), 1>(
       sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
@@ -362,7 +365,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
       [&](int it, int st) {
         const int64_t qo = (int64_t)sp.qhead(it) * N * D;
         const T* const src[2] = {Q + qo, dO + qo};
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N, wl);
+        copy.issue(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N);
       },
       [&](int it, int rs, int ts) {
         (void)it;
@@ -644,9 +647,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
   const T* const src[4] = {K + kvoff, V + kvoff, UK + kvoff, UV + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  const TileCopy<T, D, NW, 4> copy(wave_id());
   stream_loop<NSTAGE, tile_loads<T, D, NW, 4>()>(
       0, it_end,
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) { copy.issue(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
         const int s0 = it * kBS;
         const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
@@ -749,9 +753,10 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob3_alpha_kernel(
   const T* const src[2] = {K + kvoff, UK + kvoff};
   const int nT = (N + kBS - 1) / kBS;
   const int it_end = causal ? min(nT, (min(rb * BR + BR, N) - 1) / kBS + 1) : nT;
+  const TileCopy<T, D, NW, 2> copy(wave_id());
   stream_loop<NSTAGE, tile_loads<T, D, NW, 2>()>(
       0, it_end,
-      [&](int it, int st) { issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[st], it * kBS, N); },
+      [&](int it, int st) { copy.issue(src, (T FB_LDS*)lds[st], it * kBS, N); },
       [&](int it, int st) {
         const int s0 = it * kBS;
         const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
@@ -902,6 +907,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   const float inv_scale = 1.0f / scale;
   const int nTh = nT - it_begin;
   const StreamSplit<kGQA, KS, kParts> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, ks, bh, grp, part, nparts};
+  const TileCopy<T, D, NW, 3> copy(wl);
   stream_loop_rs<NSTAGE, tile_loads<T, D, NW, 3>(), 2>(
       sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(wl) == 0,
       [&](int it, int rs) {
@@ -913,7 +919,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
       [&](int it, int st) {
         const int64_t qo = (int64_t)sp.qhead(it) * N * D;
         const T* const src[3] = {Q + qo, UQ + qo, dO + qo};
-        issue_tiles<T, D, NW>(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N, wl);
+        copy.issue(src, (T FB_LDS*)lds[ks][st], sp.tile(it) * kBS, N);
       },
       [&](int it, int rs, int ts) {
         (void)it;
