@@ -3,15 +3,21 @@
 
 One step is one pass of the whole hot path over one batch of synthetic
 inputs already resident in HBM: attn_fwd_lse -> attn_bwd -> BoB Pass 1 ->
-BoB Pass 2, all on one stream.  The headline `value` is BoB TFLOP/s:
-38*B*H*N^2*d executed MFMA FLOPs (Pass 1 does 11 and Pass 2 does 8 tile
-contractions of 2*N^2*d each) divided by the time of Pass 1 + Pass 2,
+BoB Pass 2, all on one stream.  The headline `value` is BoB TFLOP/s: the
+MFMA FLOPs the two BoB passes execute, 36*B*H*N^2*d (Pass 1 runs 10 tile
+contractions of 2*N^2*d, since the first-backward dQ replaces its R
+accumulator, and Pass 2 runs 8), divided by the time of Pass 1 + Pass 2,
 measured with HIP events around the two passes inside every timed step
-(median over steps).  `ms_per_step` is the wall time of the whole step.
+(median over steps).  The paper's nominal count, 38*B*H*N^2*d (11 + 8
+contractions, Alg. 2), is reported beside it.  `ms_per_step` is the wall time
+of the whole step.
 
 Prints ONE JSON line.  Default workload: B=1, H=16, N=16384, d=128, bf16
-(Q, K ~ 0.5*N(0,1), the rest N(0,1), seed 2).  Under the causal mask the FLOP
-counts use the N(N+1)/2 unmasked (query, key) pairs per head instead of N^2.
+(Q, K ~ 0.5*N(0,1), the rest N(0,1), seed 2); the line also carries the same
+figures for the other bf16 benchmark configurations (B2 H8 N4096 d64, B1 H8
+N65536 d64, B1 H4 N262144 d64), timed for a few steps each after the
+default one.  Under the causal mask the FLOP counts use the N(N+1)/2
+unmasked (query, key) pairs per head instead of N^2.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --peak-n     # longest N (B=H=1, d=64) under a 60 s BoB cap
@@ -37,9 +43,15 @@ HBM_PEAK_GBS = 8000.0
 
 # executed MFMA FLOPs per (b, h) in units of N^2 * d, per library call.  Pass 1
 # runs 10 of the 11 tile contractions of the paper's Pass 1 because dQ is
-# passed in (R is not accumulated); the headline still counts the paper's 38.
+# passed in (R is not accumulated): the BoB passes execute 36, the paper's
+# nominal count is 38.
 FLOP_COEF = {"fwd": 4, "bwd": 14, "pass1": 20, "pass2": 16}
+BOB_COEF = FLOP_COEF["pass1"] + FLOP_COEF["pass2"]
 NOMINAL_BOB_COEF = 38
+# The other bf16 benchmark configurations the default run also times, with
+# (timed steps, warmup steps) each.
+OTHER_CONFIGS = {"bf16_b2h8_n4096_d64": (20, 3), "bf16_b1h8_n65536_d64": (5, 1),
+                 "bf16_b1h4_n262144_d64": (3, 1)}
 
 KERNEL_SOURCES = ["fb_common.h", "fb_kernels.h", "fb_launch.h", "flashbob.hip", "fb_passes_d128.hip"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
@@ -171,16 +183,16 @@ def identity_checks(x, out):
         "I3": abs(ip(x["Q"], out["Qt"]) - ip(x["K"], out["Kt"]) - (dKUK - dQUQ)) * sq
         / (nrm(x["Q"]) * nrm(out["Qt"]) + nrm(x["K"]) * nrm(out["Kt"]) + sQ + sK),
     }
-    for name, key in (("Kt", "I5"), ("Vt", "I6")):
+    for name, key in (("Kt", "I5"), ("Vt", "I6"), ("dK", "dK_colsum")):
         t = out[name].double().flatten(0, 1)
         res[key] = float((t.sum(1).norm(dim=-1) / t.norm(dim=(1, 2))).max())
     return res
 
 
-IDENTITY_TOL = {"I1": 5e-3, "I2": 5e-3, "I3": 5e-3}
-# I5, I6 are reported, not gating, in the sweep: beyond N ~ 2^19 a one-sided
-# rounding bias of the MFMA fp32 accumulation (~1e-5 per element) adds up N
-# times in a column sum; the long-N GPU test checks columns against the oracle.
+# Every identity gates the peak-N sweep: I1-I3 relative to the size of an
+# inner product of unrelated tensors, the zero column sums of Kt, Vt (I5, I6)
+# and dK relative to the matrix norm.
+IDENTITY_TOL = {"I1": 5e-3, "I2": 5e-3, "I3": 5e-3, "I5": 1e-2, "I6": 1e-2, "dK_colsum": 1e-2}
 
 
 class Path:
@@ -221,9 +233,11 @@ class Path:
 def peak_n_sweep(args, log):
     """Double N from 2^18 (B=H=1, d=64, bf16, dense) while the BoB time
     (Pass 1 + Pass 2) stays within the cap and the buffers fit in HBM; every N
-    is checked with the identities I1-I3 on its full outputs (I5, I6 are
-    reported).  Stops before running an N whose predicted BoB time (4x the
-    previous) exceeds the cap."""
+    is checked with the identities I1-I3, I5, I6 and sum_j dK_j = 0 on its
+    full outputs.  The oracle check of sampled rows and columns at the same
+    N, seed and layout is tests/test_gpu_peak_n.py (N = 2^19 ... 2^22).
+    Stops before running an N whose predicted BoB time (4x the previous)
+    exceeds the cap."""
     import torch
     import paper_2609_24089_amd as fb
     from workloads import Workload, workload_inputs
@@ -249,7 +263,7 @@ def peak_n_sweep(args, log):
         bob_s = per[2] + per[3]
         res = identity_checks(x, path.outputs())
         ok = all(res[k] <= IDENTITY_TOL[k] for k in IDENTITY_TOL)
-        tf = NOMINAL_BOB_COEF * float(N) ** 2 * 64 / bob_s / 1e12
+        tf = BOB_COEF * float(N) ** 2 * 64 / bob_s / 1e12
         ent = {"N": N, "bob_s": round(bob_s, 3), "step_s": round(sum(per), 3), "bob_tflops": round(tf, 1),
                "identities": {k: float(f"{v:.2e}") for k, v in res.items()}, "identities_ok": ok,
                "within_cap": bob_s <= args.peak_n_cap}
@@ -264,7 +278,9 @@ def peak_n_sweep(args, log):
             break
         N *= 2
     line = {"metric": f"peak N on one GPU: longest N (B=H=1, d=64, bf16, dense) whose BoB (Pass 1 + Pass 2) "
-                      f"finishes within {args.peak_n_cap:.0f} s and passes identities I1-I3",
+                      f"finishes within {args.peak_n_cap:.0f} s and passes identities I1-I3, I5, I6 and "
+                      f"sum_j dK_j = 0 (sampled rows and columns against the oracle: tests/test_gpu_peak_n.py)",
+            "bob_tflops": "executed MFMA FLOPs, 36*N^2*d",
             "value": best, "unit": "tokens", "cap_s": args.peak_n_cap,
             "hbm_bytes_per_token": 16 * 64 * 2 + 16,
             "hbm_total_gib": round(total / 2**30, 1),
@@ -327,6 +343,48 @@ def ablation(args, log):
     print(json.dumps(line), flush=True)
 
 
+DEFAULT_WORKLOAD = "bf16_b1h16_n16384_d128"
+
+
+def time_steps(torch, path, steps, warmup, dev):
+    """Run `warmup` untimed and `steps` timed steps of the path; returns the
+    per-call HIP-event times {fwd, bwd, pass1, pass2: [ms per step]} and the
+    wall time of the timed steps (s), bracketed by device synchronizations."""
+    mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    for _ in range(warmup):
+        path.step(mk())
+    events = [mk() for _ in range(steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for k in range(steps):
+        path.step(events[k])
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    names = ("fwd", "bwd", "pass1", "pass2")
+    return {n: [ev[i].elapsed_time(ev[i + 1]) for ev in events] for i, n in enumerate(names)}, wall
+
+
+def time_config(fb, torch, w, steps, warmup, dev, log):
+    """BoB time and TFLOP/s of one more benchmark configuration (a few steps)."""
+    from workloads import workload_inputs
+    log(f"configuration {w.name}: generating inputs, {steps} timed steps")
+    x = {k: v.to(dev) for k, v in workload_inputs(w).items()}
+    path = Path(fb, torch, x, w, dev)
+    per, wall = time_steps(torch, path, steps, warmup, dev)
+    bob = statistics.median(a + b for a, b in zip(per["pass1"], per["pass2"]))
+    unit = w.B * w.H * pair_count(w.N, w.causal) * w.d
+    peak = PEAK_TFLOPS[w.dtype]
+    tf = BOB_COEF * unit / (bob * 1e-3) / 1e12
+    out = {"B": w.B, "H": w.H, "N": w.N, "d": w.d, "steps": steps, "warmup": warmup,
+           "bob_ms": round(bob, 4), "bob_tflops": round(tf, 2), "pct_peak": round(100 * tf / peak, 2),
+           "bob_tflops_nominal38": round(NOMINAL_BOB_COEF * unit / (bob * 1e-3) / 1e12, 2),
+           "ms_per_step": round(wall / steps * 1e3, 4),
+           "kernels_ms": {n: round(statistics.median(v), 4) for n, v in per.items()}}
+    del path, x
+    torch.cuda.empty_cache()
+    return out
+
+
 def peak_n_summary():
     """The committed peak-N sweep, if it was taken on the current kernels."""
     try:
@@ -343,8 +401,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="bf16_b1h16_n16384_d128")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time only --workload, not the other benchmark configurations")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (counter calibration)")
@@ -388,28 +448,19 @@ def main():
         del src, dst
         log(f"copy calibration: {args.copy_calibration_mib} MiB read + written")
 
-    mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(5)]
     torch.cuda.reset_peak_memory_stats(dev)
     log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        path.step(mk())
-    events = [mk() for _ in range(args.steps)]
-    torch.cuda.synchronize(dev)
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        path.step(events[k])
-    torch.cuda.synchronize(dev)
-    wall = time.perf_counter() - t0
+    per, wall = time_steps(torch, path, args.steps, args.warmup, dev)
     log(f"timed {args.steps} steps in {wall:.2f} s")
+    peak_mem = torch.cuda.max_memory_allocated(dev)
 
     names = ("fwd", "bwd", "pass1", "pass2")
-    per = {n: [ev[i].elapsed_time(ev[i + 1]) for ev in events] for i, n in enumerate(names)}
     bob_ms = sorted(a + b for a, b in zip(per["pass1"], per["pass2"]))
     q = lambda xs, f: xs[min(len(xs) - 1, int(f * len(xs)))]
     bob_med = statistics.median(bob_ms)
     unit = w.B * w.H * pair_count(w.N, w.causal) * w.d
     peak = PEAK_TFLOPS[w.dtype]
-    value = NOMINAL_BOB_COEF * unit / (bob_med * 1e-3) / 1e12
+    value = BOB_COEF * unit / (bob_med * 1e-3) / 1e12
     kern = {}
     for n in names:
         mean_ms = statistics.mean(per[n])
@@ -427,7 +478,8 @@ def main():
     nsq = "N(N+1)/2" if w.causal else "N^2"
 
     line = {
-        "metric": "BoB TFLOP/s (38*B*H*N^2*d / time of Pass 1 + Pass 2) and % of MI355X dense bf16 MFMA peak",
+        "metric": "BoB TFLOP/s (executed MFMA FLOPs of Pass 1 + Pass 2, 36*B*H*N^2*d, / their time) and % of "
+                  "MI355X dense bf16 MFMA peak at N=16K-262K; peak N on 1 GPU",
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -444,14 +496,16 @@ def main():
         "pct_peak": round(100.0 * value / peak, 2),
         "bob_ms": {"median": round(bob_med, 4), "p20": round(q(bob_ms, 0.2), 4),
                    "p80": round(q(bob_ms, 0.8), 4)},
+        "bob_tflops_nominal38": round(NOMINAL_BOB_COEF * unit / (bob_med * 1e-3) / 1e12, 2),
+        "pct_peak_nominal38": round(100.0 * NOMINAL_BOB_COEF * unit / (bob_med * 1e-3) / 1e12 / peak, 2),
         "bob_tflops_min_count": round(24.0 * unit / (bob_med * 1e-3) / 1e12, 2),
-        "bob_tflops_executed": round((FLOP_COEF["pass1"] + FLOP_COEF["pass2"]) * unit / (bob_med * 1e-3) / 1e12, 2),
-        "flop_count": f"value counts 38*B*H*{nsq}*d (the paper's 19 tile contractions per Alg. 2); the kernels "
-                      f"executes 36 (Pass 1 takes dQ and skips R); bob_tflops_executed uses 36, "
-                      f"bob_tflops_min_count 24",
+        "flop_count": f"value and pct_peak count the executed MFMA FLOPs, 36*B*H*{nsq}*d (Pass 1 takes the "
+                      f"first-backward dQ and skips the R contraction: 10 + 8 tile contractions); the paper's "
+                      f"nominal 38 (11 + 8, Alg. 2) is bob_tflops_nominal38, the closed-form minimum 24 "
+                      f"bob_tflops_min_count",
         "step_tflops": round(step_flops / (wall / args.steps) / 1e12, 2),
         "kernels": kern,
-        "peak_mem_gib": round(torch.cuda.max_memory_allocated(dev) / 2**30, 3),
+        "peak_mem_gib": round(peak_mem / 2**30, 3),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic},
     }
@@ -470,6 +524,11 @@ def main():
             "source": src + "; scope of the timing unstated",
             "paper_ms": ref, "this_bob_ms": round(bob_med, 3), "this_step_ms": round(wall / args.steps * 1e3, 3),
             "bob_speedup": round(ref / bob_med, 2), "step_speedup": round(ref / (wall / args.steps * 1e3), 2)}
+    if not args.no_configs and args.workload == DEFAULT_WORKLOAD:
+        del path, x
+        torch.cuda.empty_cache()
+        line["configs"] = {name: time_config(fb, torch, WORKLOADS[name], steps, warm, dev, log)
+                           for name, (steps, warm) in OTHER_CONFIGS.items()}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle for about {args.cpu_seconds} s")
         line["cpu_baseline"] = cpu_baseline(x_cpu, w, budget_s=args.cpu_seconds)

@@ -480,7 +480,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
 // ===========================================================================
 enum Pass1Form : int { kSixAcc = 0, kWithDQ = 1, kAlphaGiven = 2 };
 
-template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm, int DSPLIT, bool kPF>
+template <typename T, int D, int MR, int NW, int OCC, int NSTAGE, int kForm, int DSPLIT, int kPF>
 __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ O, const T* __restrict__ dO, const T* __restrict__ UQ,
@@ -553,24 +553,45 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         s[sb][mb] = f[sb][mb] = cc[sb][mb] = floatx4{0.f, 0.f, 0.f, 0.f};
         dp[sb][mb] = floatx4{-drow[mb], -drow[mb], -drow[mb], -drow[mb]};  // the dP tile starts at -D
       }
+    // one score step: the five contractions of chunk kk of sub-block sb
+    auto step = [&](int sb, int kk, const u32x4 (&a)[4]) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < G::kChunks; ++kk) {
-        const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-        const u32x4 ak = *(const u32x4 FB_LDS*)(Ks + off);
-        const u32x4 av = *(const u32x4 FB_LDS*)(Vs + off);
-        const u32x4 auk = *(const u32x4 FB_LDS*)(UKs + off);
-        const u32x4 auv = *(const u32x4 FB_LDS*)(UVs + off);
-#pragma unroll
-        for (int mb = 0; mb < MR; ++mb) {
-          s[sb][mb] = E::mma_chunk(ak, qf[mb][kk], s[sb][mb]);        // S^T = K Q^T
-          dp[sb][mb] = E::mma_chunk(av, dof[mb][kk], dp[sb][mb]);     // (dP - D)^T = V dO^T - D
-          f[sb][mb] = E::mma_chunk(ak, uqf[mb][kk], f[sb][mb]);       // (U_Q K^T)^T
-          f[sb][mb] = E::mma_chunk(auk, qf[mb][kk], f[sb][mb]);       // + (Q U_K^T)^T
-          cc[sb][mb] = E::mma_chunk(auv, dof[mb][kk], cc[sb][mb]);    // C^T = U_V dO^T
-        }
+      for (int mb = 0; mb < MR; ++mb) {
+        s[sb][mb] = E::mma_chunk(a[0], qf[mb][kk], s[sb][mb]);        // S^T = K Q^T
+        dp[sb][mb] = E::mma_chunk(a[1], dof[mb][kk], dp[sb][mb]);     // (dP - D)^T = V dO^T - D
+        f[sb][mb] = E::mma_chunk(a[0], uqf[mb][kk], f[sb][mb]);       // (U_Q K^T)^T
+        f[sb][mb] = E::mma_chunk(a[2], qf[mb][kk], f[sb][mb]);        // + (Q U_K^T)^T
+        cc[sb][mb] = E::mma_chunk(a[3], dof[mb][kk], cc[sb][mb]);     // C^T = U_V dO^T
       }
+    };
+    auto read = [&](int sb, int kk, u32x4 (&a)[4]) {
+      const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+      a[0] = *(const u32x4 FB_LDS*)(Ks + off);
+      a[1] = *(const u32x4 FB_LDS*)(Vs + off);
+      a[2] = *(const u32x4 FB_LDS*)(UKs + off);
+      a[3] = *(const u32x4 FB_LDS*)(UVs + off);
+    };
+    if constexpr (kPF >= 2) {
+      // operands of step st + 1 are read before the MFMAs of step st
+      constexpr int kSteps = 2 * G::kChunks;
+      u32x4 nx[4];
+      read(0, 0, nx);
+#pragma unroll
+      for (int st = 0; st < kSteps; ++st) {
+        const u32x4 a[4] = {nx[0], nx[1], nx[2], nx[3]};
+        if (st + 1 < kSteps) read((st + 1) / G::kChunks, (st + 1) % G::kChunks, nx);
+        step(st / G::kChunks, st % G::kChunks, a);
+      }
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int kk = 0; kk < G::kChunks; ++kk) {
+          u32x4 a[4];
+          read(sb, kk, a);
+          step(sb, kk, a);
+        }
+    }
   };
   // s holds exponents s*tau*log2e - L*log2e (masked entries -inf)
   auto elementwise = [&]() {

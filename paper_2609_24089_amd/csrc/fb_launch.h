@@ -20,7 +20,9 @@ namespace fb {
 // stationary rows), OCC = waves per SIMD the register budget is held to, ST =
 // LDS pipeline stages (tiles in flight + 1), DS = workgroups that share one
 // row block, each accumulating 1/DS of the head dims (Pass 1 only), PF = 1 to
-// read the accumulate operands one block ahead (Pass 1 and Pass 2).
+// read the accumulate operands one block ahead (Pass 1 and Pass 2; Pass 2
+// then also reads its score operands one step ahead), 2 to also read Pass 1's
+// score operands one step ahead.
 // kColsF and kP2F are the shapes of the column kernels' two-level
 // (sectioned) accumulation for long streams (SectionSums), which holds a
 // second set of key-side sums; mr = 0 where that form is not built.
@@ -327,7 +329,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   if (dQ != nullptr) {
     constexpr Shape c = Cfg<T, D>::kP1;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ, c.ds, c.pf != 0>), dim3(g.total, c.ds),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kWithDQ, c.ds, c.pf>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)dQ,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -335,7 +337,7 @@ int32_t launch_pass1(const Problem& p, const void* Q, const void* K, const void*
   } else {
     constexpr Shape c = Cfg<T, D>::kP1Six;
     const Grid g = grid_for(p, 16 * c.mr * c.nw);
-    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc, c.ds, c.pf != 0>), dim3(g.total, c.ds),
+    hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kSixAcc, c.ds, c.pf>), dim3(g.total, c.ds),
                        dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)O,
                        (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr,
                        (const float*)nullptr, (T*)Qt, (T*)dOt, alpha, E, (int)p.N, g.nRB, g.total, p.scale,
@@ -364,7 +366,7 @@ int32_t launch_rows3(const Problem& p, const void* Q, const void* K, const void*
   constexpr Shape c = Cfg<T, D>::kP1;
   const Grid g = grid_for(p, 16 * c.mr * c.nw);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds, c.pf != 0>), dim3(g.total, c.ds),
+  hipLaunchKernelGGL((bob_pass1_kernel<T, D, c.mr, c.nw, c.occ, c.st, kAlphaGiven, c.ds, c.pf>), dim3(g.total, c.ds),
                      dim3(64 * c.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)nullptr,
                      (const T*)dO, (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, (const T*)nullptr, alpha,
                      (T*)Qt, (T*)dOt, (float*)nullptr, E, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p));
