@@ -99,18 +99,16 @@ def kernel_source_hash(read=None):
 
 
 def measured_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None if there is none for this kernel/workload or the sources changed."""
+    """HBM bytes per launch of `kernel` (fwd, bwd, pass1, pass2) at `workload`
+    from the committed rocprofv3 counter summary, or None if there is none or
+    the kernel sources have changed since the counters were taken."""
     try:
         doc = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     if doc.get("source_hash") != kernel_source_hash():
         return None
-    ent = doc.get("kernels", {}).get(kernel, {})
-    if ent.get("workload") != workload:
-        return None
-    return ent.get("bytes_per_launch")
+    return doc.get("kernels", {}).get(workload, {}).get(kernel, {}).get("bytes_per_launch")
 
 
 def cpu_baseline(x_cpu, w, slab=2048, budget_s=12.0):
@@ -375,11 +373,17 @@ def time_config(fb, torch, w, steps, warmup, dev, log):
     unit = w.B * w.H * pair_count(w.N, w.causal) * w.d
     peak = PEAK_TFLOPS[w.dtype]
     tf = BOB_COEF * unit / (bob * 1e-3) / 1e12
+    dom = max(("pass1", "pass2"), key=lambda n: statistics.mean(per[n]))
+    dom_ms = statistics.mean(per[dom])
+    achieved = FLOP_COEF[dom] * unit / (dom_ms * 1e-3) / 1e12
     out = {"B": w.B, "H": w.H, "N": w.N, "d": w.d, "steps": steps, "warmup": warmup,
            "bob_ms": round(bob, 4), "bob_tflops": round(tf, 2), "pct_peak": round(100 * tf / peak, 2),
            "bob_tflops_nominal38": round(NOMINAL_BOB_COEF * unit / (bob * 1e-3) / 1e12, 2),
            "ms_per_step": round(wall / steps * 1e3, 4),
-           "kernels_ms": {n: round(statistics.median(v), 4) for n, v in per.items()}}
+           "kernels_ms": {n: round(statistics.median(v), 4) for n, v in per.items()},
+           "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
+                        "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                        "traffic": measured_traffic(dom, w.name)}}
     del path, x
     torch.cuda.empty_cache()
     return out
