@@ -45,6 +45,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 // forward: growth of a row maximum (log2 units) that forces a rescale
 constexpr float kRescaleLog2 = 8.f;
+constexpr float kRescaleP = 256.f;   // 2^kRescaleLog2
 constexpr int kBS = 32;  // streamed rows per tile (two 16-row MFMA sub-blocks)
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
@@ -403,6 +404,21 @@ __device__ __forceinline__ void mask_tile(floatx4 (&x)[2][M], int s0, int t0, in
         const bool ok = sr < N && (!causal || (kRowMajor ? sr <= t : sr >= t));
         x[sb][m][r] = ok ? x[sb][m][r] : -INFINITY;
       }
+    }
+}
+
+// mask_tile for one stationary 16-row block: x[sb][r] belongs to streamed row
+// s0 + 16 sb + 4 (l >> 4) + r and stationary row t.
+template <bool kRowMajor>
+__device__ __forceinline__ void mask_tile1(floatx4 (&x)[2], int s0, int t, int N, bool causal) {
+  const int g = lane_id() >> 4;
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int sr = s0 + 16 * sb + 4 * g + r;
+      const bool ok = sr < N && (!causal || (kRowMajor ? sr <= t : sr >= t));
+      x[sb][r] = ok ? x[sb][r] : -INFINITY;
     }
 }
 

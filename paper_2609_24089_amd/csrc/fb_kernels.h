@@ -68,40 +68,59 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
   floatx4 s[2][MR];
   typename E::TFrag pf[MR];
 
-  // s holds log2-domain scores (masked entries -inf) when this runs
-  auto softmax_step = [&]() {
+  // Online softmax against a lazily moved reference row maximum mrun (log2
+  // domain).  The fast path forms p = exp2(s c - mrun) directly and checks
+  // that no lane's eight p exceed 2^8 in sum (so every exponent is <= 8 and
+  // p <= 256: exact in fp32 and fine in bf16; a NaN sum fails the check as
+  // well); the stale reference cancels in
+  // O = sum(P v) / sum(P) and in L = mrun + log2 sum(P).  Only when some lane
+  // fails (a row grew by about 2^8 or more, or the first tile) does the slow
+  // path find the tile's row maxima, move the reference of rows that grew by
+  // more than 2^8, rescale their output accumulators and row sums, and form
+  // p again.  `mode` 2 masks invalid entries (exponent -inf, p = 0).
+  auto softmax_step = [&](int s0, int mode) {
 #pragma unroll
     for (int mb = 0; mb < MR; ++mb) {
-      float x[8];
-      float mx = -INFINITY;
+      floatx4 e[2];
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          x[4 * sb + r] = s[sb][mb][r];
-          mx = fmaxf(mx, s[sb][mb][r]);
-        }
-      mx = group_max(mx);
-      // The reference maximum only moves when some row of the wave has grown
-      // by more than 2^8: the exponents stay <= 8, P <= 256, and the stale
-      // reference cancels in O = sum(P v) / sum(P) and in L = m + log2 sum(P).
-      // Most tiles then skip the rescale of the output accumulators.
-      if (__builtin_amdgcn_ballot_w64(mx > mrun[mb] + kRescaleLog2) != 0) {
-        const float mnew = fmaxf(mrun[mb], mx);
-        const float corr = fast_exp2(mrun[mb] - mnew);
-        mrun[mb] = mnew;
-        lsum[mb] *= corr;
-#pragma unroll
-        for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
-      }
-      float ls = lsum[mb];
+        for (int r = 0; r < 4; ++r) e[sb][r] = __builtin_fmaf(s[sb][mb][r], c, -mrun[mb]);
+      if (mode == 2) mask_tile1<true>(e, s0, row0 + 16 * mb + j, N, causal != 0);
+      float p[8], ls = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float p = fast_exp2(x[i] - mrun[mb]);
-        ls += p;
-        pf[mb].set(i, p);
+        p[i] = fast_exp2(e[i >> 2][i & 3]);
+        ls += p[i];
       }
-      lsum[mb] = ls;
+      if (__builtin_amdgcn_ballot_w64(!(ls <= kRescaleP)) != 0) {
+        // some row grew: tile maxima of the valid entries (in log2 units)
+        floatx4 x[2];
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) x[sb] = s[sb][mb] * c;
+        if (mode == 2) mask_tile1<true>(x, s0, row0 + 16 * mb + j, N, causal != 0);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) mx = fmaxf(mx, x[i >> 2][i & 3]);
+        mx = group_max(mx);
+        if (__builtin_amdgcn_ballot_w64(mx > mrun[mb] + kRescaleLog2) != 0) {
+          const float mnew = fmaxf(mrun[mb], mx);
+          const float corr = fast_exp2(mrun[mb] - mnew);
+          mrun[mb] = mnew;
+          lsum[mb] *= corr;
+#pragma unroll
+          for (int nb = 0; nb < G::kNB; ++nb) acc[nb][mb] *= corr;
+        }
+        ls = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          p[i] = fast_exp2(x[i >> 2][i & 3] - mrun[mb]);
+          ls += p[i];
+        }
+      }
+      lsum[mb] += ls;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pf[mb].set(i, p[i]);
     }
   };
 
@@ -130,12 +149,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_fwd_kernel(
 #pragma unroll
             for (int mb = 0; mb < MR; ++mb) s[sb][mb] = E::mma_chunk(a, qf[mb][kk], s[sb][mb]);
           }
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int mb = 0; mb < MR; ++mb) s[sb][mb] *= c;
-        if (mode == 2) mask_tile<true>(s, s0, row0 + j, N, causal != 0);
-        softmax_step();
+        softmax_step(s0, mode);
 #pragma unroll
         for (int nb = 0; nb < G::kNB; ++nb) {
           const typename E::AFrag a = G::load_afrag(Vs, 16 * nb);
