@@ -150,3 +150,103 @@ def test_automatic_choice(fb):
     torch.cuda.synchronize()
     for k in OUTS:
         assert torch.equal(auto[k], forced[k]), k
+
+
+def test_automatic_workspace_is_bounded(fb):
+    """The automatic split only triggers on grids smaller than about 8 jobs
+    per CU, so its workspace (parts x 2 x B*Hkv*N*d fp32) stays bounded as N
+    grows: at most 8 x CUs x (key rows per workgroup) x 2 x d x 4 bytes for
+    the parts plus one block's rounding, whatever N (multi-query, causal and
+    dense, d = 64 and 128, N = 2^10 ... 2^22)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    worst = 0
+    for d in (64, 128):
+        for causal in (False, True):
+            for logn in range(10, 23):
+                for kernel in (fb.BOB_COLUMNS_BWD, fb.BOB_COLUMNS_PASS2):
+                    lay, nbytes = fb.column_layout(kernel, torch.bfloat16, 1, 16, 1, 1 << logn, d, causal)
+                    worst = max(worst, nbytes)
+                    bound = 2 * 8 * cus * 128 * 2 * d * 4
+                    assert nbytes <= bound, (d, causal, logn, kernel, lay, nbytes)
+    say(f"[column split] largest automatic workspace over the sweep: {worst / 2**20:.0f} MiB on {cus} CUs")
+
+
+def test_long_causal_multi_query_split_and_footprint(fb):
+    """Causal multi-query attention at N = 65536 (B1, 16 query heads sharing
+    one key/value head, d = 64), where both column kernels split each block
+    over several workgroups: row-owned outputs on 16 uniformly sampled query
+    rows of every head (and row 0, whose Qt is exactly zero, against the
+    bound of its one bf16 rounding) and column-owned outputs on 32 sampled key rows (summed over the
+    query heads, given the GPU's row scalars, which the row check covers)
+    against the oracle, and the identities I1-I3, I5, I6.  Footprint: the first
+    backward adds exactly its workspace to the device memory in use, Pass 1
+    nothing beyond its outputs, and Pass 2 exactly its workspace."""
+    from tests.parity_util import check_identities
+    B, H, Hkv, N, d, causal = 1, 16, 1, 65536, 64, True
+    G = H // Hkv
+    scale = d ** -0.5
+    x = make_gqa_inputs(B, H, Hkv, N, d, "bf16", 193)
+    xd = {k: v.cuda() for k, v in x.items()}
+    Q, K, V, dO, UQ, UK, UV = (xd[n] for n in NAMES)
+    lays = {k: fb.column_layout(k, torch.bfloat16, B, H, Hkv, N, d, causal) for k in (fb.BOB_COLUMNS_BWD,
+                                                                                     fb.BOB_COLUMNS_PASS2)}
+    say(f"[column split] long causal MQA N={N}: layouts {lays}")
+    assert all(lay.parts >= 2 for lay, _ in lays.values())
+    O, L = fb.attn_fwd_lse(Q, K, V, scale, causal)
+    outs_b = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(K), torch.empty_like(L))
+    outs_1 = (torch.empty_like(Q), torch.empty_like(Q), torch.empty_like(L), torch.empty_like(L))
+    outs_2 = (torch.empty_like(K), torch.empty_like(K))
+
+    def extra(fn):
+        torch.cuda.synchronize()
+        before = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        fn()
+        torch.cuda.synchronize()
+        return torch.cuda.max_memory_allocated() - before
+
+    eb = extra(lambda: fb.attn_bwd(Q, K, V, O, dO, L, scale, causal, out=outs_b))
+    dQ, dK, dV, D = outs_b
+    e1 = extra(lambda: fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, scale, causal, dQ=dQ, out=outs_1))
+    Qt, dOt, al, E = outs_1
+    e2 = extra(lambda: fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, causal, out=outs_2))
+    say(f"   extra device memory: bwd {eb >> 20} MiB, Pass 1 {e1}, Pass 2 {e2 >> 20} MiB; alpha + E "
+        f"{(al.nbytes + E.nbytes) >> 20} MiB")
+    assert eb == lays[fb.BOB_COLUMNS_BWD][1] and e1 == 0 and e2 == lays[fb.BOB_COLUMNS_PASS2][1]
+    assert al.nbytes + E.nbytes == 2 * 4 * B * H * N
+    out = dict(O=O, L=L, D=D, dQ=dQ, dK=dK, dV=dV, Qt=Qt, dOt=dOt, alpha=al, E=E, Kt=outs_2[0], Vt=outs_2[1])
+    head = lambda h: [as_f64(x[n][0, h // G if n in ("K", "V", "UK", "UV") else h]) for n in NAMES]
+    rng = np.random.default_rng(3101)
+    row_keys = ("Qt", "dOt", "alpha", "E", "O", "L", "D", "dQ")
+    got, want = {k: [] for k in row_keys}, {k: [] for k in row_keys}
+    for h in range(H):
+        rows = np.unique(rng.choice(N, size=16, replace=False))
+        ref = oracle.bob_rows(*head(h), scale, rows, causal=causal)
+        idx = torch.as_tensor(rows, device=Q.device)
+        for k in row_keys:
+            got[k].append(as_f64(out[k][0, h].index_select(0, idx)))
+            want[k].append(ref[k])
+        # Row 0 sees key 0 only, where Qt is exactly 0: what remains is the
+        # rounding of the one bf16 operand P Pt0 = C_00 (times tau k_0) that
+        # the affine form's Omega - E0 B cancels against its fp32 row sum, at
+        # most 2^-8 |C_00| |k_0| tau, with |C_00| <= |dO_0| |U_V,0|.
+        q, k0, v, do, uq, uk, uv = head(h)
+        ref0 = oracle.bob_rows(q, k0, v, do, uq, uk, uv, scale, np.array([0]), causal=causal)
+        bound = 2.0 ** -8 * scale * np.linalg.norm(do[0]) * np.linalg.norm(uv[0]) * np.linalg.norm(k0[0])
+        assert np.abs(ref0["Qt"]).max() == 0.0
+        assert np.linalg.norm(as_f64(out["Qt"][0, h, 0]) - ref0["Qt"][0]) <= bound, h
+    errs = {k: nrel(np.concatenate(got[k]), np.concatenate(want[k])) for k in row_keys}
+    cols = np.sort(np.random.default_rng(3102).choice(N, size=32, replace=False))
+    acc = {k: 0.0 for k in COLUMN_OUTS}
+    for h in range(H):
+        rs = {k: as_f64(out[k][0, h]) for k in ("alpha", "E", "L", "D")}
+        ref = oracle.bob_cols(*head(h), scale, cols, rs["alpha"], rs["E"], rs["L"], rs["D"], causal=causal)
+        for k in COLUMN_OUTS:
+            acc[k] = acc[k] + ref[k]
+    idx = torch.as_tensor(cols, device=Q.device)
+    for k in COLUMN_OUTS:
+        errs[k] = nrel(as_f64(out[k][0, 0].index_select(0, idx)), acc[k])
+    say("   errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, e in errs.items():
+        assert e <= TOL["bf16"], (k, e)
+    check_identities(xd, out)
