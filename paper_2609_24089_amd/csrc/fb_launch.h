@@ -38,13 +38,13 @@ template <> struct Cfg<bf16, 32> {
   static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2};
 };
 template <> struct Cfg<bf16, 64> {
-  static constexpr Shape kFwd{2, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
+  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 2, 2};
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr Shape kFwd{1, 8, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
+  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
   static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1};
