@@ -102,7 +102,7 @@ typedef enum {
  *               column sums of Kt, Vt, dK grow with N); in sections, each
  *               chain restarts from zero and is added into fp32 sums with
  *               round-to-nearest adds.  Automatic: sections of 1024 tiles
- *               when a chain would exceed 8192 tiles (bf16 d <= 128; other
+ *               when a chain would exceed 16384 tiles (bf16 d <= 128; other
  *               (dtype, d) run one section, and asking for sections there
  *               gives BOB_EUNSUPPORTED).
  * Different layouts sum in different orders, so results differ in the last

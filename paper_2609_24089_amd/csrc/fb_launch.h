@@ -41,7 +41,7 @@ template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 2, 2};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2};
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
@@ -158,9 +158,10 @@ inline Grid grid_for(const Problem& p, int rows_per_block, bool kv_heads = false
 constexpr int kMaxParts = 8;
 // Automatic sections: a stream longer than kLongChain tiles per accumulator
 // chain is cut into sections of kSectionTiles.  Measured on the zero column
-// sums (B1 H1 d64 bf16): at chains of 8192 tiles the residual stays at the
-// bf16 rounding floor, at 32768 and above it is over three times the floor.
-constexpr int64_t kLongChain = 8192;
+// sums (B1 H1 d64 bf16): at chains of 16384 tiles the residual stays at the
+// bf16 rounding floor (about 3e-3), at 32768 it is 8.8e-3 and at 65536
+// 2.9e-2; in sections of 1024 it stays at the floor up to N = 2^22.
+constexpr int64_t kLongChain = 16384;
 constexpr int kSectionTiles = 1024;
 
 struct ColumnOpts {

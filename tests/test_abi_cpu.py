@@ -281,11 +281,11 @@ def test_column_layout_resolves_requests(lib):
         for d in (32, 64, 128):
             assert layout(lib, kernel, opts(1, 1), H=1, N=1 << 20, d=d, causal=0) == ((1, 1, 1024), 0)
             assert layout(lib, kernel, opts(1, 1, -1), H=1, N=1 << 20, d=d, causal=0) == ((1, 1, -1), 0)
-            # 8192 tiles stay in one chain; split in 8 parts the chain is short again
-            assert layout(lib, kernel, opts(1, 1), H=1, N=1 << 18, d=d, causal=0) == ((1, 1, -1), 0)
+            # 16384 tiles stay in one chain; split in 8 parts the chain is short again
+            assert layout(lib, kernel, opts(1, 1), H=1, N=1 << 19, d=d, causal=0) == ((1, 1, -1), 0)
             assert layout(lib, kernel, opts(8, 1), H=1, N=1 << 20, d=d, causal=0)[0] == (8, 1, -1)
-        # grouped heads lengthen the stream: 16 query heads x 1024 tiles
-        assert layout(lib, kernel, opts(1, 1), H=16, Hkv=1, N=32768, d=64, causal=0)[0] == (1, 1, 1024)
+        # grouped heads lengthen the stream: 16 query heads x 2048 tiles
+        assert layout(lib, kernel, opts(1, 1), H=16, Hkv=1, N=65536, d=64, causal=0)[0] == (1, 1, 1024)
     # the empty problem has the trivial layout
     assert layout(lib, fb.BOB_COLUMNS_PASS2, None, N=0) == ((1, 1, -1), 0)
 

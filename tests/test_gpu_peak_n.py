@@ -12,7 +12,7 @@ configuration the benchmark times, at N = 2^19 ... 2^22:
 
 The column sums are what a one-signed rounding error in a long accumulation
 shows: every column adds it, so the sum over N columns grows like N while
-the norm it is compared with grows like sqrt(N).  Above 8192 streamed tiles
+the norm it is compared with grows like sqrt(N).  Above 16384 streamed tiles
 per accumulator chain the column kernels accumulate in sections of 1024
 tiles (bob_column_opts.flush_tiles, automatic), which keeps these sums at the
 bf16 rounding floor; the test checks that the automatic layout does so."""
@@ -40,8 +40,8 @@ def test_long_sequence(logn):
     for kernel, name in ((fb.BOB_COLUMNS_BWD, "bwd"), (fb.BOB_COLUMNS_PASS2, "pass2")):
         got, _ = fb.column_layout(kernel, torch.bfloat16, 1, 1, 1, N, 64, False)
         say(f"[peak-n] N={N} {name} column layout {got}")
-        # more than 8192 streamed tiles per chain -> sections of 1024
-        assert got.flush_tiles == (1024 if N // 32 > 8192 * got.parts * got.wave_sets else -1)
+        # more than 16384 streamed tiles per chain -> sections of 1024
+        assert got.flush_tiles == (1024 if N // 32 > 16384 * got.parts * got.wave_sets else -1)
     say(f"[peak-n] {w.name}: generating inputs")
     x = workload_inputs(w)
     xd = to_dev(x)
