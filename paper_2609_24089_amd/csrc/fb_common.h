@@ -297,12 +297,11 @@ __device__ __forceinline__ void load_stationary(u32x4 (&f)[NC], const T* head, i
   }
 }
 
-// Issue the HBM -> LDS copy of NTENS streamed tiles (rows s0 .. s0+kBS-1)
-// with global_load_lds_dwordx4: each wave instruction fills one contiguous
-// 1 KB block of the tile, lane i writing 16 bytes at offset 16*i, so the lane
-// fetches the logical chunk that belongs at that (permuted) position.  Rows
-// >= N are clamped to row N-1 (finite data); every kernel masks them out.
-// The copy is asynchronous: wait_vm<>() before the barrier that publishes it.
+// A streamed tile is copied HBM -> LDS in 1 KB blocks: each wave load
+// instruction fills one contiguous block, lane i writing 16 bytes at offset
+// 16*i, so the lane fetches the logical chunk that belongs at that (permuted)
+// position (TileCopy below).  The copy is asynchronous: wait_vm<>() before
+// the barrier that publishes it.
 // Loads each wave issues per streamed tile: the NTENS x kBlocks 1 KB blocks
 // of one tile stage are dealt out evenly over the NW waves.
 template <typename T, int D, int NW, int NTENS>
@@ -678,7 +677,7 @@ __device__ __forceinline__ void merge_wave_sets(floatx4 (&x)[A][B], floatx4 (&y)
 // Indices >= N are clamped to N-1; the kernels mask those rows.  The two base
 // pointers are passed by value so that the per-lane choice is a register
 // select (an indexed pointer array would go through scratch memory and force
-// a full vmcnt wait).  Asynchronous like issue_tiles().
+// a full vmcnt wait).  Asynchronous like the tile copy.
 __device__ __forceinline__ void issue_scalar_pair(float FB_LDS* dst, const float* a, const float* b, int s0, int N) {
   static_assert(kBS == 32, "two 32-float vectors per wave instruction");
   const int l = lane_id();

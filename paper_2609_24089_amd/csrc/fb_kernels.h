@@ -409,6 +409,9 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
             dp[sb][mc] = t1;
           }
         }
+        // the score MFMAs run at raised wave priority, so that a wave that
+        // reaches them issues them ahead of the other waves' exponentials
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
@@ -422,6 +425,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
               dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
             }
           }
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
           const floatx4 t0 = *(const floatx4 FB_LDS*)(Ts + 16 * sb + 4 * g);
@@ -1010,6 +1014,8 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
           o[1] = *(const u32x4 FB_LDS*)(UQs + off);
           o[2] = *(const u32x4 FB_LDS*)(dOs + off);
         };
+        // score MFMAs at raised wave priority, as in the first backward
+        __builtin_amdgcn_s_setprio(1);
         if constexpr (kPF) {
           // operands of step st + 1 are read before the MFMAs of step st
           constexpr int kSteps = 2 * G::kChunks;
@@ -1031,6 +1037,7 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
               score_step(sb, kk, a[0], a[1], a[2]);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         prep_next();
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
