@@ -299,7 +299,7 @@ __global__ __launch_bounds__(NW * 64, OCC) void attn_bwd_rows_kernel(
 // more workgroups than CUs).
 // ===========================================================================
 template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, bool kGQA, int KS, bool kParts = false,
-          bool kFlush = false>
+          bool kFlush = false, bool kKL = false>
 __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const T* __restrict__ dO, const float* __restrict__ L, const float* __restrict__ Dv,
@@ -312,12 +312,21 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   // The tile ring, and the raw L, D of NSTAGE tiles with two slots of
   // transformed ones: T0 = -L log2e (the exponent offset), T1 = -D (the dP
   // tile's start value).  One LDS variable, for the reason given at Pass 2's Smem2.
+  // With kKL each wave's 32 stationary K rows sit in LDS (a tile in the
+  // streamed tiles' layout, shared by the wave of the same index in each
+  // wave set) instead of registers: 32 key rows per wave then fit two waves
+  // per SIMD, which halves the LDS bytes per MFMA of the streamed tiles for
+  // 8 more b128 reads per tile.
   struct Smem {
     T lds[KS][NSTAGE][2 * G::kTileElems];
     float rawsc[KS][NSTAGE][2 * kBS];
     float tsc[KS][2][2 * kBS];
   };
-  __shared__ __attribute__((aligned(16))) Smem sm;
+  struct SmemK : Smem {
+    T kst[NW][G::kTileElems];
+  };
+  static_assert(!kKL || 16 * MC == kBS, "stationary K in LDS: one 32-row tile per wave");
+  __shared__ __attribute__((aligned(16))) std::conditional_t<kKL, SmemK, Smem> sm;
   auto& lds = sm.lds;
   auto& rawsc = sm.rawsc;
   auto& tsc = sm.tsc;
@@ -333,11 +342,21 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   const int wl = KS == 1 ? wave_id() : wave_id() % NW;  // wave within its set
   const int col0 = rb * BC + wl * 16 * MC;
 
-  u32x4 kf[MC][G::kChunks], vf[MC][G::kChunks];
+  u32x4 kf[kKL ? 1 : MC][G::kChunks], vf[MC][G::kChunks];
 #pragma unroll
   for (int mc = 0; mc < MC; ++mc) {
-    load_stationary<T, D>(kf[mc], K + hoff, col0 + 16 * mc + j, N);
+    if constexpr (!kKL) load_stationary<T, D>(kf[mc], K + hoff, col0 + 16 * mc + j, N);
     load_stationary<T, D>(vf[mc], V + hoff, col0 + 16 * mc + j, N);
+  }
+  if constexpr (kKL) {
+    // rows past N read as zeros; a wave whose rows all lie past N stores
+    // nothing, so its tile stays unwritten.  The first wave set copies; the
+    // loop's first wait_vm<0>() and barrier publish the tile to both.
+    if (ks == 0 && col0 < N) {
+      const TileCopy<T, D, 1, 1> kc(0);
+      const T* const ksrc[1] = {K + hoff};
+      kc.issue(ksrc, (T FB_LDS*)sm.kst[wl], col0, N);
+    }
   }
   floatx4 dk[G::kNB][MC], dv[G::kNB][MC];
 #pragma unroll
@@ -412,19 +431,41 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
         // the score MFMAs run at raised wave priority, so that a wave that
         // reaches them issues them ahead of the other waves' exponentials
         __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        if constexpr (kKL) {
+          // each K chunk is read once per tile and serves both sub-blocks
+          const T FB_LDS* Ks = (const T FB_LDS*)sm.kst[wl];
 #pragma unroll
           for (int kk = 0; kk < G::kChunks; ++kk) {
-            const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
-            const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
-            const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+            u32x4 kfr[MC];
 #pragma unroll
-            for (int mc = 0; mc < MC; ++mc) {
-              s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);
-              dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
+            for (int mc = 0; mc < MC; ++mc) kfr[mc] = *(const u32x4 FB_LDS*)(Ks + G::chunk_off(16 * mc + j, 4 * kk + g));
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+              const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+              const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+              const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+              for (int mc = 0; mc < MC; ++mc) {
+                s[sb][mc] = E::mma_chunk(aq, kfr[mc], s[sb][mc]);
+                dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
+              }
             }
           }
+        } else {
+#pragma unroll
+          for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int kk = 0; kk < G::kChunks; ++kk) {
+              const int off = G::chunk_off(16 * sb + j, 4 * kk + g);
+              const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+              const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+#pragma unroll
+              for (int mc = 0; mc < MC; ++mc) {
+                s[sb][mc] = E::mma_chunk(aq, kf[mc][kk], s[sb][mc]);
+                dp[sb][mc] = E::mma_chunk(ado, vf[mc][kk], dp[sb][mc]);
+              }
+            }
+        }
         __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {

@@ -22,12 +22,13 @@ namespace fb {
 // row block, each accumulating 1/DS of the head dims (Pass 1 only), PF = 1 to
 // read the accumulate operands one block ahead (Pass 1 and Pass 2; Pass 2
 // then also reads its score operands one step ahead), 2 to also read Pass 1's
-// score operands one step ahead.
+// score operands one step ahead.  KL = 1 keeps the first backward column
+// kernel's stationary K rows in LDS instead of registers (with MR = 2).
 // kColsF and kP2F are the shapes of the column kernels' two-level
 // (sectioned) accumulation for long streams (SectionSums), which holds a
 // second set of key-side sums; mr = 0 where that form is not built.
 struct Shape {
-  int mr, nw, occ, st, ds = 1, pf = 0;
+  int mr, nw, occ, st, ds = 1, pf = 0, kl = 0;
 };
 constexpr Shape kNoForm{0, 1, 1, 2};
 template <typename T, int D> struct Cfg;
@@ -38,13 +39,13 @@ template <> struct Cfg<bf16, 32> {
   static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2};
 };
 template <> struct Cfg<bf16, 64> {
-  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
+  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2};
 };
 template <> struct Cfg<bf16, 128> {
-  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{1, 4, 2, 2};
+  static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1};
@@ -187,11 +188,12 @@ inline bool resolve_two_sets(int requested, int workgroups) {
   return workgroups <= device_cus();
 }
 
-template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, int NTENS, int NSCAL>
+template <typename T, int D, int MC, int NW, int OCC, int NSTAGE, int NTENS, int NSCAL, bool KL = false>
 constexpr bool two_sets_fit() {
   constexpr size_t ring = (size_t)NSTAGE * NTENS * Geo<T, D>::kTileElems * sizeof(T);
   constexpr size_t scal = (size_t)(NSTAGE + 2) * NSCAL * kBS * sizeof(float);
-  return OCC == 2 && 2 * (ring + scal) <= 160 * 1024 &&
+  constexpr size_t kst = KL ? (size_t)NW * Geo<T, D>::kTileElems * sizeof(T) : 0;  // shared by both sets
+  return OCC == 2 && 2 * (ring + scal) + kst <= 160 * 1024 &&
          2 * ring >= (size_t)NW * Geo<T, D>::kNB * MC * 1024;
 }
 
@@ -210,7 +212,7 @@ struct ColumnShape {
   static constexpr Shape kS =
       kPass2 ? (kF ? Cfg<T, D>::kP2F : Cfg<T, D>::kP2) : (kF ? Cfg<T, D>::kColsF : Cfg<T, D>::kCols);
   static constexpr bool kTwoFit =
-      kS.mr > 0 && two_sets_fit<T, D, kS.mr, kS.nw, kS.occ, kS.st, kPass2 ? 3 : 2, kPass2 ? 4 : 2>();
+      kS.mr > 0 && two_sets_fit<T, D, kS.mr, kS.nw, kS.occ, kS.st, kPass2 ? 3 : 2, kPass2 ? 4 : 2, kS.kl != 0>();
 };
 
 // Plan of a validated, non-empty, supported problem.  BOB_EINVAL for a
@@ -269,7 +271,7 @@ int32_t launch_bwd_cols(const Problem& p, const void* Q, const void* K, const vo
     (void)hipGetLastError();
     if (cp.parts > 1) {
       // each column block split over cp.parts workgroups, then one reduction
-      hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true, 1, true, kF>),
+      hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, true, 1, true, kF, cc.kl != 0>),
                          dim3(gc.total * cp.parts), dim3(64 * cc.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V,
                          (const T*)dO, L, Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale, p.causal,
                          group(p), parts_ws, cp.parts, cp.flush_tiles);
@@ -281,7 +283,7 @@ int32_t launch_bwd_cols(const Problem& p, const void* Q, const void* K, const vo
     }
     auto cols = [&](auto gqa, auto ks) {
       hipLaunchKernelGGL((attn_bwd_cols_kernel<T, D, cc.mr, cc.nw, cc.occ, cc.st, decltype(gqa)::value,
-                                               decltype(ks)::value, false, kF>),
+                                               decltype(ks)::value, false, kF, cc.kl != 0>),
                          dim3(gc.total), dim3(64 * cc.nw * decltype(ks)::value), 0, s, (const T*)Q, (const T*)K,
                          (const T*)V, (const T*)dO, L, Dv, (T*)dK, (T*)dV, (int)p.N, gc.nRB, gc.total, p.scale,
                          p.causal, group(p), (float*)nullptr, 1, cp.flush_tiles);

@@ -129,9 +129,10 @@ def test_automatic_choice(fb):
         got = ws_bytes(fb, True, fb.BOB_BF16, 1, 16, Hkv, N, d, causal)
         say(f"[column split] auto Hkv={Hkv} causal={causal} CUs {cus}: {got} bytes (parts {parts})")
         assert got == want, (Hkv, causal, got, want)
-        # the first backward's column kernel also owns 64 key rows per
-        # workgroup here, and is split to about 8 jobs per CU under either mask
-        pb = min(8, -(-8 * cus // grid(Hkv)))
+        # the first backward's column kernel owns 128 key rows per workgroup
+        # here (32 per wave), and is split to about 8 jobs per CU under
+        # either mask
+        pb = min(8, -(-8 * cus // (Hkv * (N // 128))))
         want_b = 0 if pb < 2 else pb * 2 * Hkv * N * d * 4
         assert ws_bytes(fb, False, fb.BOB_BF16, 1, 16, Hkv, N, d, causal) == want_b, (Hkv, causal)
     # short blocks (fewer than 1024 streamed iterations) are never split
