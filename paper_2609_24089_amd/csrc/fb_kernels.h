@@ -312,20 +312,23 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
   // The tile ring, and the raw L, D of NSTAGE tiles with two slots of
   // transformed ones: T0 = -L log2e (the exponent offset), T1 = -D (the dP
   // tile's start value).  One LDS variable, for the reason given at Pass 2's Smem2.
-  // With kKL each wave's 32 stationary K rows sit in LDS (a tile in the
-  // streamed tiles' layout, shared by the wave of the same index in each
-  // wave set) instead of registers: 32 key rows per wave then fit two waves
-  // per SIMD, which halves the LDS bytes per MFMA of the streamed tiles for
-  // 8 more b128 reads per tile.
+  // With kKL the stationary K rows sit in LDS instead of registers, in
+  // 32-row tiles of the streamed tiles' layout: one per wave at 32 key rows
+  // per wave (MC = 2), one per pair of consecutive waves at 16 (MC = 1),
+  // shared by the waves of the same index in each wave set.  At d <= 128 the
+  // freed registers let a wave own 32 key rows at two waves per SIMD, which
+  // halves the LDS bytes per MFMA of the streamed tiles for 8 more b128 reads
+  // per tile; at d = 256 they let 16 rows per wave run at two waves per SIMD.
   struct Smem {
     T lds[KS][NSTAGE][2 * G::kTileElems];
     float rawsc[KS][NSTAGE][2 * kBS];
     float tsc[KS][2][2 * kBS];
   };
+  constexpr int kWPT = kBS / (16 * MC);  // waves per stationary K tile
+  static_assert(!kKL || (kBS % (16 * MC) == 0 && NW % kWPT == 0), "stationary K in LDS: 32-row tiles");
   struct SmemK : Smem {
-    T kst[NW][G::kTileElems];
+    T kst[NW / kWPT][G::kTileElems];
   };
-  static_assert(!kKL || 16 * MC == kBS, "stationary K in LDS: one 32-row tile per wave");
   __shared__ __attribute__((aligned(16))) std::conditional_t<kKL, SmemK, Smem> sm;
   auto& lds = sm.lds;
   auto& rawsc = sm.rawsc;
@@ -352,10 +355,10 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
     // rows past N read as zeros; a wave whose rows all lie past N stores
     // nothing, so its tile stays unwritten.  The first wave set copies; the
     // loop's first wait_vm<0>() and barrier publish the tile to both.
-    if (ks == 0 && col0 < N) {
+    if (ks == 0 && wl % kWPT == 0 && col0 < N) {
       const TileCopy<T, D, 1, 1> kc(0);
       const T* const ksrc[1] = {K + hoff};
-      kc.issue(ksrc, (T FB_LDS*)sm.kst[wl], col0, N);
+      kc.issue(ksrc, (T FB_LDS*)sm.kst[wl / kWPT], col0, N);
     }
   }
   floatx4 dk[G::kNB][MC], dv[G::kNB][MC];
@@ -433,12 +436,14 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void attn_bwd_cols_kernel(
         __builtin_amdgcn_s_setprio(1);
         if constexpr (kKL) {
           // each K chunk is read once per tile and serves both sub-blocks
-          const T FB_LDS* Ks = (const T FB_LDS*)sm.kst[wl];
+          const T FB_LDS* Ks = (const T FB_LDS*)sm.kst[wl / kWPT];
+          const int r0 = 16 * MC * (wl % kWPT);  // the wave's first row in the tile
 #pragma unroll
           for (int kk = 0; kk < G::kChunks; ++kk) {
             u32x4 kfr[MC];
 #pragma unroll
-            for (int mc = 0; mc < MC; ++mc) kfr[mc] = *(const u32x4 FB_LDS*)(Ks + G::chunk_off(16 * mc + j, 4 * kk + g));
+            for (int mc = 0; mc < MC; ++mc)
+              kfr[mc] = *(const u32x4 FB_LDS*)(Ks + G::chunk_off(r0 + 16 * mc + j, 4 * kk + g));
 #pragma unroll
             for (int sb = 0; sb < 2; ++sb) {
               const int off = G::chunk_off(16 * sb + j, 4 * kk + g);

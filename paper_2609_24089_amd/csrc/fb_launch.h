@@ -23,7 +23,7 @@ namespace fb {
 // read the accumulate operands one block ahead (Pass 1 and Pass 2; Pass 2
 // then also reads its score operands one step ahead), 2 to also read Pass 1's
 // score operands one step ahead.  KL = 1 keeps the first backward column
-// kernel's stationary K rows in LDS instead of registers (with MR = 2).
+// kernel's stationary K rows in LDS instead of registers.
 // kColsF and kP2F are the shapes of the column kernels' two-level
 // (sectioned) accumulation for long streams (SectionSums), which holds a
 // second set of key-side sums; mr = 0 where that form is not built.
@@ -51,7 +51,7 @@ template <> struct Cfg<bf16, 128> {
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1};
 };
 template <> struct Cfg<bf16, 256> {
-  static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 4, 1, 2};
+  static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 8, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 1, 2, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
   static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
