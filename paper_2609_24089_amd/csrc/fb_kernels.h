@@ -741,6 +741,9 @@ __global__ __launch_bounds__(NW * 64, OCC) void bob_pass1_kernel(
         const int mode = tile_mode_rowmajor(s0, row0, row0 + 16 * MR - 1, N, causal != 0);
         if (mode == 0) return;
         const T FB_LDS* Ks = (const T FB_LDS*)lds[st];
+        // bf16 d = 128: LLVM's exp-interleave scheduling strategy for the tile
+        // (Pass 1 1.1-1.5% faster; slower at d = 64)
+        if constexpr (std::is_same_v<T, bf16> && D == 128) __builtin_amdgcn_iglp_opt(3);
         score(Ks);
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
