@@ -95,6 +95,11 @@ typedef enum {
  *               Automatic: two when the grid has no more workgroups than the
  *               device has compute units (and the shape has room: bf16
  *               d <= 128, fp32 Pass 2 with d <= 64); a split block uses one.
+ *               On a dense unsplit grid that fills the device, the
+ *               automatic bf16 d = 128 Pass 2 runs one set in workgroups of
+ *               twice the waves (one copy of each streamed tile serves
+ *               more key rows), with results equal bit for bit to those of
+ *               a forced wave_sets = 1.
  *  flush_tiles  streamed tiles per accumulation section, >= 1, or -1 for one
  *               section.  The MFMA's fp32 accumulation drops the low bits of
  *               small addends toward one side, so a chain of tens of

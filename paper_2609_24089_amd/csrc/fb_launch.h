@@ -26,7 +26,10 @@ namespace fb {
 // kernel's stationary K rows in LDS instead of registers.
 // kColsF and kP2F are the shapes of the column kernels' two-level
 // (sectioned) accumulation for long streams (SectionSums), which holds a
-// second set of key-side sums; mr = 0 where that form is not built.
+// second set of key-side sums; mr = 0 where that form is not built.  kP2W
+// is Pass 2 in wide workgroups (more waves sharing one copy of each streamed
+// tile, one workgroup per CU), run on grids that fill the device without
+// wave sets, parts or sections; mr = 0 where it is not built.
 struct Shape {
   int mr, nw, occ, st, ds = 1, pf = 0, kl = 0;
 };
@@ -36,43 +39,43 @@ template <> struct Cfg<bf16, 32> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{2, 4, 2, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2};
+  static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2}, kP2W = kNoForm;
 };
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2}, kP2W = kNoForm;
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1}, kP2W{1, 8, 2, 2, 1, 1};
 };
 template <> struct Cfg<bf16, 256> {
   static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 8, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 1, 2, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
 };
 template <> struct Cfg<float, 32> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
 };
 template <> struct Cfg<float, 64> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
 };
 template <> struct Cfg<float, 128> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -171,6 +174,7 @@ struct ColumnOpts {
 struct ColumnPlan {
   Grid g{0, 0};
   int parts = 1, sets = 1, flush_tiles = 0;
+  bool wide = false;   // Pass 2 in the kP2W shape
 };
 
 // Compute units of the current device (0 if it cannot be read).
@@ -193,7 +197,7 @@ constexpr bool two_sets_fit() {
   constexpr size_t ring = (size_t)NSTAGE * NTENS * Geo<T, D>::kTileElems * sizeof(T);
   constexpr size_t scal = (size_t)(NSTAGE + 2) * NSCAL * kBS * sizeof(float);
   constexpr size_t kst = KL ? (size_t)NW * Geo<T, D>::kTileElems * sizeof(T) : 0;  // shared by both sets
-  return OCC == 2 && 2 * (ring + scal) + kst <= 160 * 1024 &&
+  return OCC == 2 && NW <= 4 && 2 * (ring + scal) + kst <= 160 * 1024 &&
          2 * ring >= (size_t)NW * Geo<T, D>::kNB * MC * 1024;
 }
 
@@ -243,6 +247,22 @@ int32_t plan_columns(const Problem& p, const ColumnOpts& o, ColumnPlan* out) {
     if (SF::kS.mr == 0) return BOB_EUNSUPPORTED;
     c = fill(SF::kS, SF::kTwoFit);
     c.flush_tiles = ft;
+  }
+  // Wide Pass 2 workgroups on dense grids that fill every CU with them
+  // (under the causal mask the larger blocks balance worse), when the wave
+  // sets are automatic: 3-4% faster at N = 16384, d = 128 with 16 and with 4
+  // key/value heads, outputs bit for bit those of the narrow form (each wave
+  // does the same arithmetic), which a forced wave_sets = 1 still runs.
+  if constexpr (kPass2 && Cfg<T, D>::kP2W.mr > 0) {
+    constexpr Shape w = Cfg<T, D>::kP2W;
+    const int cus = device_cus();
+    if (o.wave_sets == 0 && !p.causal && c.parts == 1 && c.sets == 1 && c.flush_tiles <= 0 && cus > 0) {
+      const Grid gw = grid_for(p, 16 * w.mr * w.nw, true);
+      if (gw.total >= cus) {
+        c.g = gw;
+        c.wide = true;
+      }
+    }
   }
   *out = c;
   return BOB_OK;
@@ -400,6 +420,20 @@ int32_t launch_pass2_form(const Problem& p, const void* Q, const void* K, const 
                          cp.parts, plane, p.scale, p.scale, (T*)Kt, (T*)Vt);
       return finish_launch();
     }
+    const bool gqa = group(p) != 1;
+    if constexpr (!kF && Cfg<T, D>::kP2W.mr > 0) {
+      constexpr Shape w = Cfg<T, D>::kP2W;
+      auto wide = [&](auto kv) {
+        hipLaunchKernelGGL((bob_pass2_kernel<T, D, w.mr, w.nw, w.occ, w.st, decltype(kv)::value, 1, w.pf != 0>),
+                           dim3(g.total), dim3(64 * w.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
+                           (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N,
+                           g.nRB, g.total, p.scale, p.causal, group(p), (float*)nullptr, 1, 0);
+      };
+      if (cp.wide) {
+        gqa ? wide(std::true_type{}) : wide(std::false_type{});
+        return finish_launch();
+      }
+    }
     auto pass2 = [&](auto gqa, auto ks) {
       hipLaunchKernelGGL((bob_pass2_kernel<T, D, c.mr, c.nw, c.occ, c.st, decltype(gqa)::value, decltype(ks)::value,
                                            c.pf != 0, false, kF>),
@@ -408,7 +442,6 @@ int32_t launch_pass2_form(const Problem& p, const void* Q, const void* K, const 
                          (T*)Kt, (T*)Vt, (int)p.N, g.nRB, g.total, p.scale, p.causal, group(p), (float*)nullptr, 1,
                          cp.flush_tiles);
     };
-    const bool gqa = group(p) != 1;
     if constexpr (ColumnShape<T, D, true, kF>::kTwoFit) {
       if (cp.sets == 2) {
         gqa ? pass2(std::true_type{}, std::integral_constant<int, 2>{})

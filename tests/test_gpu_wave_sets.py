@@ -6,7 +6,9 @@ checked against the float64 oracle on multi-head and grouped problems, dense
 and causal, with iteration counts that are odd (the second set's last
 iteration has no tile) or 1 (the second set has none at all); the row-owned
 outputs must not depend on the form; and the automatic choice must pick two
-sets on a grid with no more workgroups than CUs and one set on a larger grid."""
+sets on a grid with no more workgroups than CUs and one set on a larger grid.
+The wide bf16 d = 128 Pass 2 workgroups that the automatic choice runs on
+large dense grids must give the one-set result bit for bit."""
 import numpy as np
 import pytest
 import torch
@@ -106,3 +108,27 @@ def test_each_form_is_deterministic(fb):
         b = run(fb, xd, 0.1, True, mode)
         for k in OUTS:
             assert torch.equal(a[k], b[k]), (mode, k)
+
+
+@pytest.mark.parametrize("shape", [(1, 32, 32, 2000), (1, 16, 4, 8192)], ids=["H32N2000", "H16kv4N8192"])
+def test_wide_pass2_matches_one_set(fb, shape):
+    """bf16 d = 128, dense: Pass 2 grids of at least one workgroup per CU in
+    the wide form (128 key rows per workgroup; N = 2000 ends in a partial
+    block) run wide when the wave sets are automatic and narrow (64 key rows
+    per workgroup) when one set is forced; Kt and Vt must agree bit for bit
+    (the same producers and Pass 1 outputs feed both)."""
+    B, H, Hkv, N = shape
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert column_grid(128, B, Hkv, N) >= cus
+    say(f"[wave sets] wide Pass 2 B{B} H{H} Hkv{Hkv} N{N} d128 (CUs {cus})")
+    xd = {k: v.cuda() for k, v in make_gqa_inputs(B, H, Hkv, N, 128, "bf16", 172).items()}
+    Q, K, V, dO, UQ, UK, UV = (xd[n] for n in NAMES)
+    scale = 128 ** -0.5
+    O, L = fb.attn_fwd_lse(Q, K, V, scale)
+    dQ, dK, dV, D = fb.attn_bwd(Q, K, V, O, dO, L, scale)
+    Qt, dOt, al, E = fb.attn_bob_pass1_rows(Q, K, V, O, dO, UQ, UK, UV, L, D, scale, dQ=dQ)
+    auto = fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, columns=fb.ColumnOpts(1, 0, 0))
+    one = fb.attn_bob_pass2_cols(Q, K, V, dO, UQ, UK, UV, L, D, al, E, scale, columns=fb.ColumnOpts(1, 1, 0))
+    torch.cuda.synchronize()
+    for a, b, name in zip(auto, one, ("Kt", "Vt")):
+        assert torch.equal(a, b), name
