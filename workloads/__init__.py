@@ -66,6 +66,8 @@ WORKLOADS = {
 for _d, _seed in ((32, 8), (64, 9), (128, 10), (256, 11)):
     _n = f"causal_bf16_b4h12_n4096_d{_d}"
     WORKLOADS[_n] = Workload(_n, 4, 12, 4096, _d, "bf16", _seed, causal=True)
+# Dense d=256 at N=8K (head-dim extension; 16 heads fill the device).
+WORKLOADS["bf16_b1h16_n8192_d256"] = Workload("bf16_b1h16_n8192_d256", 1, 16, 8192, 256, "bf16", 15)
 # Grouped key/value heads at the N=16K d=128 shape: 4 and 1 (multi-query) key/value heads for 16 query heads.
 for _n, _hkv, _seed, _causal in (("gqa_bf16_b1h16kv4_n16384_d128", 4, 12, False),
                                  ("mqa_bf16_b1h16kv1_n16384_d128", 1, 13, False),
