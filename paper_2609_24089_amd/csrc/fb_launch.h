@@ -49,13 +49,13 @@ template <> struct Cfg<bf16, 64> {
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
-  static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 8, 2, 3, 2}, kP2{1, 4, 2, 2, 1, 1};
+  static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1}, kP2W{1, 8, 2, 2, 1, 1};
 };
 template <> struct Cfg<bf16, 256> {
   static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 8, 2, 2, 1, 0, 1};
-  static constexpr Shape kP1{1, 4, 1, 2, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
+  static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
   static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
 };
