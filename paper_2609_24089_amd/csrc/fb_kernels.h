@@ -1154,6 +1154,228 @@ __global__ __launch_bounds__(KS * NW * 64, OCC) void bob_pass2_kernel(
   }
 }
 
+// ===========================================================================
+// BoB Pass 2 (as bob_pass2_kernel) in wave pairs, for head dims whose
+// stationary rows and key-side sums do not fit one wave at two waves per
+// SIMD (bf16 d = 256: K, V, U_K, U_V fragments and the Kt, Vt sums of 16
+// key rows take 256 registers).  The two waves of a pair own the same 16
+// key rows and split the head dims: half h holds dims [h D/2, (h+1) D/2) of
+// the stationary rows and accumulates those dims of Kt and Vt.  Per streamed
+// tile each wave forms partial score tiles over its dims (the row terms
+// enter through half 0's start values only), hands its partial sums of
+// sub-block 1 - h to the partner through LDS and adds the partner's partial
+// sums of sub-block h, so that it holds the full score tiles of one 16-row
+// sub-block.  It does the elementwise step there, hands its half of the
+// bf16 accumulate fragments to the partner, and both accumulate their dims
+// over all 32 streamed rows.  The two hand-overs add two workgroup-wide
+// barriers per tile; every wave runs them on every tile, whatever its tile
+// mode.  Waves p and p + NP form pair p; the workgroup owns 16 NP key rows.
+// ===========================================================================
+template <typename T, int D, int NP, bool kGQA>
+__global__ __launch_bounds__(2 * NP * 64, 2) void bob_pass2_pair_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const T* __restrict__ dO, const T* __restrict__ UQ, const T* __restrict__ UK,
+    const T* __restrict__ UV, const float* __restrict__ L, const float* __restrict__ Dv,
+    const float* __restrict__ alpha_in, const float* __restrict__ E_in,
+    T* __restrict__ Kt, T* __restrict__ Vt, int N, int nRB, int total, float scale, int causal, int grp) {
+  static_assert(sizeof(T) == 2, "bf16 only");
+  using E = Elt<T>;
+  using G = Geo<T, D>;
+  constexpr int NW = 2 * NP;
+  constexpr int BC = 16 * NP;
+  constexpr int kHC = G::kChunks / 2;   // score steps (32-dim chunks) per half
+  constexpr int kHB = G::kNB / 2;       // 16-dim output blocks per half
+  struct SmemPair {
+    T lds[2][3 * G::kTileElems];
+    float rawsc[2][4 * kBS];
+    float tsc[2][4 * kBS];
+    floatx4 xs[NW][4][64];   // partial score tiles handed to the partner
+    u32x2 xf[NW][3][64];     // half accumulate fragments handed to the partner
+  };
+  __shared__ __attribute__((aligned(16))) SmemPair sm;
+
+  int bh, rb;
+  map_block(nRB, total, bh, rb);
+  const int64_t hoff = (int64_t)bh * N * D;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const int w = wave_id();
+  const int pr = w % NP;
+  const int col0 = rb * BC + 16 * pr;
+  const int col = col0 + j;
+  const float c = scale * kLog2e;
+  const float inv_scale = 1.0f / scale;
+  const int nT = (N + kBS - 1) / kBS;
+  const int it_begin = causal ? (rb * BC) / kBS : 0;
+  const int nTh = nT - it_begin;
+  const StreamSplit<kGQA, 1> sp{it_begin, nTh, kGQA ? grp * nTh : nTh, 0, bh, grp};
+  const TileCopy<T, D, NW, 3> copy(w);
+
+  // The half is a compile-time constant inside run(), so every chunk, block
+  // and fragment-slot index below is static; the branch is wave-uniform.
+  auto run = [&](auto H) {
+    constexpr int h = decltype(H)::value;
+    const int partner = pr + NP * (1 - h);
+
+    // this half's chunks of the stationary rows: chunk c = kHC h + kk
+    u32x4 kf[kHC], vf[kHC], ukf[kHC], uvf[kHC];
+#pragma unroll
+    for (int kk = 0; kk < kHC; ++kk) {
+      const int64_t off = hoff + (int64_t)col * D + (kHC * h + kk) * E::kKC + g * (E::kKC / 4);
+      const bool in = col < N;
+      kf[kk] = in ? *(const u32x4*)(K + off) : u32x4{0u, 0u, 0u, 0u};
+      vf[kk] = in ? *(const u32x4*)(V + off) : u32x4{0u, 0u, 0u, 0u};
+      ukf[kk] = in ? *(const u32x4*)(UK + off) : u32x4{0u, 0u, 0u, 0u};
+      uvf[kk] = in ? *(const u32x4*)(UV + off) : u32x4{0u, 0u, 0u, 0u};
+    }
+    floatx4 aK[kHB], aV[kHB];
+#pragma unroll
+    for (int nb = 0; nb < kHB; ++nb) aK[nb] = aV[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    stream_loop_rs<2, tile_loads<T, D, NW, 3>(), 2>(
+        sp.begin(), sp.end(nT), __builtin_amdgcn_readfirstlane(w) == 0,
+        [&](int it, int rs) {
+          const int64_t qs = (int64_t)sp.qhead(it) * N;
+          float FB_LDS* dst = (float FB_LDS*)sm.rawsc[rs];
+          issue_scalar_pair(dst, L + qs, Dv + qs, sp.tile(it) * kBS, N);
+          issue_scalar_pair(dst + 2 * kBS, alpha_in + qs, E_in + qs, sp.tile(it) * kBS, N);
+        },
+        [&](int it, int st) {
+          const int64_t qo = (int64_t)sp.qhead(it) * N * D;
+          const T* const src[3] = {Q + qo, UQ + qo, dO + qo};
+          copy.issue(src, (T FB_LDS*)sm.lds[st], sp.tile(it) * kBS, N);
+        },
+        [&](int it, int rs, int ts) {
+          (void)it;
+          if (l < kBS) {
+            const float FB_LDS* raw = (const float FB_LDS*)sm.rawsc[rs];
+            float FB_LDS* t = (float FB_LDS*)sm.tsc[ts];
+            const float Lr = raw[l], Dr = raw[kBS + l], ar = raw[2 * kBS + l], Er = raw[3 * kBS + l];
+            t[l] = -Lr * kLog2e;
+            t[kBS + l] = -Dr;
+            t[2 * kBS + l] = -ar * inv_scale;
+            t[3 * kBS + l] = -__builtin_fmaf(ar, Dr, Er);
+          }
+        },
+        [&](int it, int st, int ts, auto&& prep_next) {
+          const int s0 = sp.tile(it) * kBS;
+          const int mode = tile_mode_colmajor(s0, col0, col0 + 15, N, causal != 0);
+          const T FB_LDS* Qs = (const T FB_LDS*)sm.lds[st];
+          const T FB_LDS* UQs = Qs + G::kTileElems;
+          const T FB_LDS* dOs = UQs + G::kTileElems;
+          const float FB_LDS* Ts = (const float FB_LDS*)sm.tsc[ts];
+          // partial score tiles [s = query][t = key] over this half's dims;
+          // half 0 starts from the row terms (as bob_pass2_kernel), half 1 from 0
+          floatx4 s[2], dp[2], f[2], cc[2];
+          if (mode != 0) {
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+              s[sb] = floatx4{0.f, 0.f, 0.f, 0.f};
+              if constexpr (h == 0) {
+                dp[sb] = *(const floatx4 FB_LDS*)(Ts + kBS + 16 * sb + 4 * g);
+                f[sb] = *(const floatx4 FB_LDS*)(Ts + 2 * kBS + 16 * sb + 4 * g);
+                cc[sb] = *(const floatx4 FB_LDS*)(Ts + 3 * kBS + 16 * sb + 4 * g);
+              } else {
+                dp[sb] = f[sb] = cc[sb] = floatx4{0.f, 0.f, 0.f, 0.f};
+              }
+            }
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+              for (int kk = 0; kk < kHC; ++kk) {
+                const int off = G::chunk_off(16 * sb + j, 4 * (kHC * h + kk) + g);
+                const u32x4 aq = *(const u32x4 FB_LDS*)(Qs + off);
+                const u32x4 auq = *(const u32x4 FB_LDS*)(UQs + off);
+                const u32x4 ado = *(const u32x4 FB_LDS*)(dOs + off);
+                s[sb] = E::mma_chunk(aq, kf[kk], s[sb]);        // S = Q K^T
+                dp[sb] = E::mma_chunk(ado, vf[kk], dp[sb]);     // dP - D
+                f[sb] = E::mma_chunk(auq, kf[kk], f[sb]);       // (U_Q K^T
+                f[sb] = E::mma_chunk(aq, ukf[kk], f[sb]);       //  + Q U_K^T) - alpha / tau
+                cc[sb] = E::mma_chunk(ado, uvf[kk], cc[sb]);    // C - (alpha D + E)
+              }
+          }
+          prep_next();
+          // hand-over 1: the partner finishes sub-block 1 - h
+          if (mode != 0) {
+            floatx4 FB_LDS* out = (floatx4 FB_LDS*)&sm.xs[w][0][l];
+            constexpr int ob = 1 - h;
+            out[0] = s[ob];
+            out[64] = dp[ob];
+            out[128] = f[ob];
+            out[192] = cc[ob];
+          }
+          __syncthreads();
+          typename E::TFrag fPh, fSt, fdS;
+          if (mode != 0) {
+            const floatx4 FB_LDS* in = (const floatx4 FB_LDS*)&sm.xs[partner][0][l];
+            floatx4 ts_ = s[h] + in[0], tdp = dp[h] + in[64], tf = f[h] + in[128], tcc = cc[h] + in[192];
+            const floatx4 t0 = *(const floatx4 FB_LDS*)(Ts + 16 * h + 4 * g);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ts_[r] = __builtin_fmaf(ts_[r], c, t0[r]);
+            if (mode == 2) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int sr = s0 + 16 * h + 4 * g + r;
+                const bool ok = sr < N && (causal == 0 || sr >= col);
+                ts_[r] = ok ? ts_[r] : -INFINITY;
+              }
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float pv = fast_exp2(ts_[r]);
+              const float u = tf[r];
+              const float dd = tdp[r];
+              const int i = 4 * h + r;
+              fPh.set(i, pv * u);
+              fSt.set(i, pv * __builtin_fmaf(scale, u * dd, tcc[r]));
+              fdS.set(i, pv * dd);
+            }
+            // hand-over 2: this half's slots of the three fragments
+            u32x2 FB_LDS* outf = (u32x2 FB_LDS*)&sm.xf[w][0][l];
+            const u32x4 a = __builtin_bit_cast(u32x4, fPh.v), b = __builtin_bit_cast(u32x4, fSt.v),
+                        d = __builtin_bit_cast(u32x4, fdS.v);
+            outf[0] = u32x2{a[2 * h], a[2 * h + 1]};
+            outf[64] = u32x2{b[2 * h], b[2 * h + 1]};
+            outf[128] = u32x2{d[2 * h], d[2 * h + 1]};
+          }
+          __syncthreads();
+          if (mode != 0) {
+            const u32x2 FB_LDS* inf = (const u32x2 FB_LDS*)&sm.xf[partner][0][l];
+            constexpr int o = 2 * (1 - h);
+            auto fill = [&](typename E::TFrag& fr, u32x2 x) {
+              u32x4 v = __builtin_bit_cast(u32x4, fr.v);
+              v[o] = x[0];
+              v[o + 1] = x[1];
+              fr.v = __builtin_bit_cast(bf16x8, v);
+            };
+            fill(fPh, inf[0]);
+            fill(fSt, inf[64]);
+            fill(fdS, inf[128]);
+#pragma unroll
+            for (int nb = 0; nb < kHB; ++nb) {
+              const int dim0 = 16 * (kHB * h + nb);
+              const typename E::AFrag aq = G::load_afrag(Qs, dim0);
+              const typename E::AFrag auq = G::load_afrag(UQs, dim0);
+              const typename E::AFrag ado = G::load_afrag(dOs, dim0);
+              aV[nb] = E::mma_acc(ado, fPh, aV[nb]);
+              aK[nb] = E::mma_acc(aq, fSt, aK[nb]);
+              aK[nb] = E::mma_acc(auq, fdS, aK[nb]);
+            }
+          }
+        });
+    if (col < N) {
+#pragma unroll
+      for (int nb = 0; nb < kHB; ++nb) {
+        const int64_t off = hoff + (int64_t)col * D + 16 * (kHB * h + nb) + 4 * g;
+        E::store4(Kt + off, aK[nb] * scale);
+        E::store4(Vt + off, aV[nb] * scale);
+      }
+    }
+  };
+  if (__builtin_amdgcn_readfirstlane(w) < NP)
+    run(std::integral_constant<int, 0>{});
+  else
+    run(std::integral_constant<int, 1>{});
+}
+
 // Sum of the nparts fp32 partial planes of a split column kernel (plane
 // elements each, laid out [nparts][2][plane]), in part order, times scale_k
 // (first plane of each part, into Kt) or scale_v (second, into Vt), rounded

@@ -29,7 +29,10 @@ namespace fb {
 // second set of key-side sums; mr = 0 where that form is not built.  kP2W
 // is Pass 2 in wide workgroups (more waves sharing one copy of each streamed
 // tile, one workgroup per CU), run on grids that fill the device without
-// wave sets, parts or sections; mr = 0 where it is not built.
+// wave sets, parts or sections; mr = 0 where it is not built.  kP2P is Pass
+// 2 in wave pairs that split the head dims (bob_pass2_pair_kernel, nw waves
+// = nw / 2 pairs of 16 key rows), for head dims whose one-wave form holds
+// one wave per SIMD; run where kP2W would be, dense or causal.
 struct Shape {
   int mr, nw, occ, st, ds = 1, pf = 0, kl = 0;
 };
@@ -39,43 +42,43 @@ template <> struct Cfg<bf16, 32> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
   static constexpr Shape kP1{2, 4, 2, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2}, kP2W = kNoForm;
+  static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2}, kP2W = kNoForm, kP2P = kNoForm;
 };
 template <> struct Cfg<bf16, 64> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 2, 2}, kP1Six{1, 4, 2, 2}, kP2{2, 4, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2}, kP2W = kNoForm;
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 3, 2}, kP2W = kNoForm, kP2P = kNoForm;
 };
 template <> struct Cfg<bf16, 128> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 8, 2, 2, 1, 1}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2, 1, 1};
   static constexpr Shape kAlpha{2, 4, 2, 2};
-  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1}, kP2W{1, 8, 2, 2, 1, 1};
+  static constexpr Shape kColsF{1, 4, 2, 2}, kP2F{1, 4, 1, 2, 1, 1}, kP2W{1, 8, 2, 2, 1, 1}, kP2P = kNoForm;
 };
 template <> struct Cfg<bf16, 256> {
   static constexpr Shape kFwd{1, 4, 2, 2}, kRows{1, 4, 2, 2}, kCols{1, 8, 2, 2, 1, 0, 1};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 2, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm, kP2P{1, 8, 2, 2};
 };
 template <> struct Cfg<float, 32> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm, kP2P = kNoForm;
 };
 template <> struct Cfg<float, 64> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 2, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm, kP2P = kNoForm;
 };
 template <> struct Cfg<float, 128> {
   static constexpr Shape kFwd{1, 4, 1, 2}, kRows{1, 4, 1, 2}, kCols{1, 4, 1, 2};
   static constexpr Shape kP1{1, 4, 1, 2}, kP1Six{1, 4, 1, 2}, kP2{1, 4, 1, 2};
   static constexpr Shape kAlpha{1, 4, 1, 2};
-  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm;
+  static constexpr Shape kColsF = kNoForm, kP2F = kNoForm, kP2W = kNoForm, kP2P = kNoForm;
 };
 
 constexpr int64_t kMaxN = int64_t(1) << 30;
@@ -175,6 +178,7 @@ struct ColumnPlan {
   Grid g{0, 0};
   int parts = 1, sets = 1, flush_tiles = 0;
   bool wide = false;   // Pass 2 in the kP2W shape
+  bool pairs = false;  // Pass 2 in wave pairs (kP2P)
 };
 
 // Compute units of the current device (0 if it cannot be read).
@@ -262,6 +266,16 @@ int32_t plan_columns(const Problem& p, const ColumnOpts& o, ColumnPlan* out) {
         c.g = gw;
         c.wide = true;
       }
+    }
+  }
+  // Wave pairs where the one-wave Pass 2 holds one wave per SIMD, on the
+  // same unsplit, single-set, one-section layouts (the pairs' column blocks
+  // have the one-wave form's 16 key rows per pair).
+  if constexpr (kPass2 && Cfg<T, D>::kP2P.mr > 0) {
+    constexpr Shape q = Cfg<T, D>::kP2P;
+    if (o.wave_sets == 0 && c.parts == 1 && c.sets == 1 && c.flush_tiles <= 0) {
+      c.g = grid_for(p, 16 * (q.nw / 2), true);
+      c.pairs = true;
     }
   }
   *out = c;
@@ -431,6 +445,19 @@ int32_t launch_pass2_form(const Problem& p, const void* Q, const void* K, const 
       };
       if (cp.wide) {
         gqa ? wide(std::true_type{}) : wide(std::false_type{});
+        return finish_launch();
+      }
+    }
+    if constexpr (!kF && Cfg<T, D>::kP2P.mr > 0) {
+      constexpr Shape q = Cfg<T, D>::kP2P;
+      auto pairs = [&](auto kv) {
+        hipLaunchKernelGGL((bob_pass2_pair_kernel<T, D, q.nw / 2, decltype(kv)::value>), dim3(g.total),
+                           dim3(64 * q.nw), 0, s, (const T*)Q, (const T*)K, (const T*)V, (const T*)dO,
+                           (const T*)UQ, (const T*)UK, (const T*)UV, L, Dv, alpha, E, (T*)Kt, (T*)Vt, (int)p.N,
+                           g.nRB, g.total, p.scale, p.causal, group(p));
+      };
+      if (cp.pairs) {
+        gqa ? pairs(std::true_type{}) : pairs(std::false_type{});
         return finish_launch();
       }
     }
