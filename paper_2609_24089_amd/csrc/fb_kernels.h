@@ -1266,6 +1266,8 @@ __global__ __launch_bounds__(2 * NP * 64, 2) void bob_pass2_pair_kernel(
           // half 0 starts from the row terms (as bob_pass2_kernel), half 1 from 0
           floatx4 s[2], dp[2], f[2], cc[2];
           if (mode != 0) {
+            // score MFMAs at raised wave priority, as in bob_pass2_kernel
+            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
             for (int sb = 0; sb < 2; ++sb) {
               s[sb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1291,6 +1293,7 @@ __global__ __launch_bounds__(2 * NP * 64, 2) void bob_pass2_pair_kernel(
                 f[sb] = E::mma_chunk(aq, ukf[kk], f[sb]);       //  + Q U_K^T) - alpha / tau
                 cc[sb] = E::mma_chunk(ado, uvf[kk], cc[sb]);    // C - (alpha D + E)
               }
+            __builtin_amdgcn_s_setprio(0);
           }
           prep_next();
           // hand-over 1: the partner finishes sub-block 1 - h
