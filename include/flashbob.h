@@ -99,7 +99,11 @@ typedef enum {
  *               automatic bf16 d = 128 Pass 2 runs one set in workgroups of
  *               twice the waves (one copy of each streamed tile serves
  *               more key rows), with results equal bit for bit to those of
- *               a forced wave_sets = 1.
+ *               a forced wave_sets = 1.  The automatic bf16 d = 256 Pass 2
+ *               on an unsplit block runs in wave pairs that split the head
+ *               dims and exchange partial score tiles through LDS; its
+ *               results differ from a forced wave_sets = 1 in the order of
+ *               fp32 sums inside the score tiles.
  *  flush_tiles  streamed tiles per accumulation section, >= 1, or -1 for one
  *               section.  The MFMA's fp32 accumulation drops the low bits of
  *               small addends toward one side, so a chain of tens of
