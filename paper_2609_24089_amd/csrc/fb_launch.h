@@ -40,7 +40,7 @@ constexpr Shape kNoForm{0, 1, 1, 2};
 template <typename T, int D> struct Cfg;
 template <> struct Cfg<bf16, 32> {
   static constexpr Shape kFwd{2, 4, 2, 2}, kRows{2, 4, 2, 2}, kCols{2, 4, 2, 2};
-  static constexpr Shape kP1{2, 4, 2, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
+  static constexpr Shape kP1{1, 4, 3, 2}, kP1Six{2, 4, 2, 2}, kP2{2, 2, 2, 2};
   static constexpr Shape kAlpha{2, 4, 2, 2};
   static constexpr Shape kColsF{2, 4, 2, 2}, kP2F{2, 2, 2, 2}, kP2W = kNoForm, kP2P = kNoForm;
 };
