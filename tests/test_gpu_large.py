@@ -1,4 +1,4 @@
-"""GPU checks at the three large workloads, in the launch configuration the
+"""GPU checks at the large workloads, in the launch configuration the
 benchmark times (Pass 1 with dQ, one stream):
 
 * B=1 H=16 N=16384 d=128 (Q, K ~ 0.5 N(0,1), seed 2): row-owned outputs on
@@ -18,6 +18,10 @@ benchmark times (Pass 1 with dQ, one stream):
   key row sums over all 262144 query rows, so it checks the column
   arithmetic given the row scalars, which are checked separately at the
   sampled query rows;
+* B=1 H=16 N=8192 d=256 (seed 15; Pass 1 in one workgroup per row block,
+  Pass 2 in wave pairs): row-owned outputs on 32 sampled query rows of every
+  head; column-owned outputs on 128 sampled key rows of head 0, using row
+  scalars the oracle computes for all 8192 rows of that head;
 * the identities I1-I3, I5, I6 on the full outputs of every workload;
 * footprint: the two BoB passes allocate nothing beyond caller buffers.
 Normwise bar on every sampled set: 2e-2 (bf16 inputs, fp32 accumulation)."""
@@ -38,6 +42,18 @@ def test_n16384_d128():
     check_rows(x, out, w, rows_per_head=64, seed=1002)
     say("[large] column outputs of head 0 (oracle row scalars for all rows)")
     check_cols(x, out, w, heads=[0], ncols=256, seed=2002, scalars="oracle")
+    check_identities(xd, out)
+
+
+def test_n8192_d256():
+    w = WORKLOADS["bf16_b1h16_n8192_d256"]
+    say(f"[large] {w.name}: GPU path")
+    x = workload_inputs(w)
+    xd = to_dev(x)
+    out = run_gpu_path(xd, w.scale)
+    check_rows(x, out, w, rows_per_head=32, seed=1005)
+    say("[large] column outputs of head 0 (oracle row scalars for all rows)")
+    check_cols(x, out, w, heads=[0], ncols=128, seed=2005, scalars="oracle")
     check_identities(xd, out)
 
 
